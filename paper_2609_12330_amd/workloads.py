@@ -1,0 +1,132 @@
+"""Seeded synthetic attention workloads.
+
+This module only draws inputs. It holds none of the attention arithmetic, so
+both the HIP path (through its tests and the benchmark) and the fp64 oracle
+can take their inputs from it without sharing any of the computation.
+
+Every input is drawn on the CPU from ``torch.Generator('cpu')`` seeded with
+the caller's seed: q, then k, then v, each as float32 ``randn`` of shape
+``[B, H, S, D]`` (D innermost), rounded to bfloat16 (round-to-nearest-even).
+The paper's workloads are causal multi-head attention in decode and prefill
+over Llama 2 / BERT style shapes (section 7.1, "Workloads"); its benchmark
+suites are not available, so these i.i.d. N(0, 1) tensors of the same layout
+stand in for them.
+"""
+
+from __future__ import annotations
+
+import dataclasses
+import math
+from typing import Dict, Tuple
+
+import torch
+
+
+@dataclasses.dataclass(frozen=True)
+class AttentionConfig:
+    """One attention problem: shapes, mask, softmax scale and how q is drawn."""
+
+    name: str
+    B: int
+    Hq: int
+    Hkv: int
+    Sq: int
+    Skv: int
+    D: int
+    causal: bool
+    partition_size: int = 0  # split-KV partition (tokens); 0 = unsplit / heuristic
+    q_mult: float = 1.0  # q = bf16(q_mult * N(0,1)); 2.0 sharpens the softmax
+    scale: float = dataclasses.field(default=float("nan"))
+
+    def __post_init__(self):
+        if math.isnan(self.scale):
+            object.__setattr__(self, "scale", 1.0 / math.sqrt(self.D))
+
+    @property
+    def G(self) -> int:
+        return self.Hq // self.Hkv
+
+    def visible_pairs(self) -> int:
+        """Number of (query, key) pairs the mask leaves visible, over the batch and heads."""
+        if not self.causal:
+            per_head = self.Sq * self.Skv
+        else:
+            off = self.Skv - self.Sq
+            per_head = sum(max(0, min(self.Skv, i + off + 1)) for i in range(self.Sq))
+        return self.B * self.Hq * per_head
+
+    def flops(self) -> int:
+        """Algorithmic flops: 2*D for q.k plus 2*D for p*v per visible pair."""
+        return 4 * self.D * self.visible_pairs()
+
+    def kv_bytes(self) -> int:
+        return 2 * self.B * self.Hkv * self.Skv * self.D * 2
+
+    def algorithmic_bytes(self) -> int:
+        """bf16 q, k, v read once plus the fp32 output written once."""
+        q = self.B * self.Hq * self.Sq * self.D * 2
+        o = self.B * self.Hq * self.Sq * self.D * 4
+        return q + self.kv_bytes() + o
+
+
+# The five synthetic workloads: a tiny MHA case, GQA decode with 256-token KV
+# partitions, causal GQA prefill, 131072-token decode split 512 ways with a
+# sharper softmax, and 8-token chunked decode with a bottom-right causal mask.
+CONFIGS: Tuple[AttentionConfig, ...] = (
+    AttentionConfig("tiny_mha_b1_h4_s64_d64", 1, 4, 4, 64, 64, 64, causal=False),
+    AttentionConfig("gqa_decode_b8_h32x8_kv4096_d128", 8, 32, 8, 1, 4096, 128, causal=False,
+                    partition_size=256),
+    AttentionConfig("causal_gqa_prefill_b4_h32x8_s2048_d128", 4, 32, 8, 2048, 2048, 128,
+                    causal=True),
+    AttentionConfig("long_decode_b1_h32x8_kv131072_d128", 1, 32, 8, 1, 131072, 128, causal=False,
+                    partition_size=256, q_mult=2.0),
+    AttentionConfig("chunked_decode_b16_h64x8_q8_kv8192_d128", 16, 64, 8, 8, 8192, 128,
+                    causal=True),
+)
+
+CONFIG_BY_NAME: Dict[str, AttentionConfig] = {c.name: c for c in CONFIGS}
+
+# Default seed of each workload: its position in CONFIGS, counted from 1.
+DEFAULT_SEED: Dict[str, int] = {c.name: i + 1 for i, c in enumerate(CONFIGS)}
+
+
+def make_inputs(cfg: AttentionConfig, seed: int):
+    """Draw bf16 q [B,Hq,Sq,D], k and v [B,Hkv,Skv,D] on the CPU, in that order."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(int(seed))
+    q = torch.randn(cfg.B, cfg.Hq, cfg.Sq, cfg.D, generator=g, dtype=torch.float32)
+    k = torch.randn(cfg.B, cfg.Hkv, cfg.Skv, cfg.D, generator=g, dtype=torch.float32)
+    v = torch.randn(cfg.B, cfg.Hkv, cfg.Skv, cfg.D, generator=g, dtype=torch.float32)
+    if cfg.q_mult != 1.0:
+        q = q * cfg.q_mult
+    return q.to(torch.bfloat16), k.to(torch.bfloat16), v.to(torch.bfloat16)
+
+
+def make_shape_inputs(B, Hq, Hkv, Sq, Skv, D, seed, q_mult=1.0):
+    """Same recipe as :func:`make_inputs` for an arbitrary shape."""
+    cfg = AttentionConfig("adhoc", B, Hq, Hkv, Sq, Skv, D, causal=False, q_mult=q_mult)
+    return make_inputs(cfg, seed)
+
+
+def to_f64(t: torch.Tensor):
+    """Widen a (bf16) CPU tensor to a float64 numpy array; exact for bf16 values."""
+    return t.detach().to("cpu", torch.float64).numpy()
+
+
+def make_partials(rows: int, P: int, D: int, seed: int, empty_frac: float = 0.0):
+    """Random fp32 split-KV partial states (m, l, acc) for testing a combine step.
+
+    ``m`` ~ 4*N(0,1), ``l`` ~ U(0.5, 64), ``acc`` ~ N(0,1) * l; a fraction
+    ``empty_frac`` of the (row, partition) slots is the empty state (-inf, 0, 0).
+    """
+    g = torch.Generator(device="cpu")
+    g.manual_seed(int(seed))
+    m = 4.0 * torch.randn(rows, P, generator=g, dtype=torch.float32)
+    l = 0.5 + 63.5 * torch.rand(rows, P, generator=g, dtype=torch.float32)
+    acc = torch.randn(rows, P, D, generator=g, dtype=torch.float32) * l[:, :, None]
+    if empty_frac > 0.0:
+        empty = torch.rand(rows, P, generator=g) < empty_frac
+        m[empty] = float("-inf")
+        l[empty] = 0.0
+        acc[empty] = 0.0
+    return m, l, acc

@@ -1,0 +1,495 @@
+"""Pins for the fp64 oracle: what the definition and the mathematics fix.
+
+The paper prints no numeric attention example, so the oracle is pinned by
+hand-derived closed forms (tests/golden), closed-form special cases,
+invariants of softmax attention, torch's scaled_dot_product_attention in fp64
+on the CPU (an independent library routine), and pure-Python brute force.
+The mutation tests at the end plant plausible mistakes in the oracle and check
+that at least one pin catches each.
+"""
+
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import oracle.attention as oa
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "closed_form_cases.json")
+
+RNG_SHAPES = [
+    # B, Hq, Hkv, Sq, Skv, D
+    (1, 1, 1, 1, 1, 4),
+    (1, 2, 1, 5, 9, 8),
+    (2, 4, 2, 7, 7, 8),
+    (1, 8, 2, 3, 33, 16),
+    (2, 2, 2, 9, 4, 4),  # Sq > Skv: causal rows with nothing visible
+]
+
+
+def _rand(shape, seed, scale=1.0):
+    return np.random.default_rng(seed).standard_normal(shape) * scale
+
+
+def _inputs(B, Hq, Hkv, Sq, Skv, D, seed):
+    q = _rand((B, Hq, Sq, D), seed)
+    k = _rand((B, Hkv, Skv, D), seed + 1)
+    v = _rand((B, Hkv, Skv, D), seed + 2)
+    return q, k, v
+
+
+def _visible_count(Sq, Skv, causal):
+    if not causal:
+        return np.full(Sq, Skv)
+    return np.array([max(0, min(Skv, i + Skv - Sq + 1)) for i in range(Sq)])
+
+
+def _sdpa64(q, k, v, scale, causal):
+    """torch SDPA in fp64 on the CPU with an explicit bottom-right mask, GQA enabled."""
+    Sq, Skv = q.shape[2], k.shape[2]
+    tq, tk, tv = (torch.from_numpy(np.ascontiguousarray(x)) for x in (q, k, v))
+    mask = None
+    if causal:
+        i = torch.arange(Sq)[:, None]
+        j = torch.arange(Skv)[None, :]
+        mask = j <= i + (Skv - Sq)
+    out = torch.nn.functional.scaled_dot_product_attention(
+        tq, tk, tv, attn_mask=mask, scale=scale, enable_gqa=True)
+    return out.numpy()
+
+
+# ---------------------------------------------------------------------------
+# Pin checks, written against an attention implementation `impl(q,k,v,scale,causal)`
+# so the mutation tests can run them on deliberately broken variants.
+# Each returns the max deviation from what the pin fixes.
+# ---------------------------------------------------------------------------
+
+
+def dev_golden(impl):
+    cases = json.load(open(GOLDEN))["attention"]
+    consts = {"ln3": math.log(3.0), "ln2/2": math.log(2.0) / 2, "ln2": math.log(2.0)}
+
+    def val(x):
+        if isinstance(x, list):
+            return [val(y) for y in x]
+        return consts[x] if isinstance(x, str) else float(x)
+
+    worst = 0.0
+    for c in cases:
+        o = impl(np.array(val(c["q"])), np.array(val(c["k"])), np.array(val(c["v"])),
+                 val(c["scale"]), c["causal"])
+        worst = max(worst, float(np.max(np.abs(o - np.array(val(c["o"]))))))
+    return worst
+
+
+def dev_constant_v(impl):
+    """Every value row equal to one vector c (per kv head): every visible output row is c."""
+    worst = 0.0
+    for n, (B, Hq, Hkv, Sq, Skv, D) in enumerate(RNG_SHAPES):
+        q, k, _ = _inputs(B, Hq, Hkv, Sq, Skv, D, 10 + n)
+        c = _rand((B, Hkv, 1, D), 99 + n)
+        v = np.broadcast_to(c, (B, Hkv, Skv, D)).copy()
+        for causal in (False, True):
+            o = impl(q, k, v, 0.7, causal)
+            G = Hq // Hkv
+            want = np.repeat(c, G, axis=1)
+            vis = _visible_count(Sq, Skv, causal) > 0
+            worst = max(worst, float(np.max(np.abs(o[:, :, vis] - want))))
+            if (~vis).any():
+                worst = max(worst, float(np.max(np.abs(o[:, :, ~vis]))))
+    return worst
+
+
+def dev_uniform_logits(impl):
+    """q = 0: every visible key gets equal weight, so O[i] is the mean of the visible v rows."""
+    worst = 0.0
+    for n, (B, Hq, Hkv, Sq, Skv, D) in enumerate(RNG_SHAPES):
+        _, k, v = _inputs(B, Hq, Hkv, Sq, Skv, D, 20 + n)
+        q = np.zeros((B, Hq, Sq, D))
+        G = Hq // Hkv
+        for causal in (False, True):
+            o = impl(q, k, v, 1.3, causal)
+            cnt = _visible_count(Sq, Skv, causal)
+            for i in range(Sq):
+                for hq in range(Hq):
+                    want = v[:, hq // G, :cnt[i]].mean(axis=1) if cnt[i] else 0.0
+                    worst = max(worst, float(np.max(np.abs(o[:, hq, i] - want))))
+    return worst
+
+
+def dev_one_hot(impl):
+    """Logits that single out key j*: q = a e_0, k_j* = e_0, other keys orthogonal -> O = v_j*."""
+    worst = 0.0
+    Skv, D = 12, 8
+    for jstar in (0, 5, 11):
+        k = np.zeros((1, 1, Skv, D))
+        k[0, 0, :, 1] = 1.0
+        k[0, 0, jstar] = 0.0
+        k[0, 0, jstar, 0] = 1.0
+        q = np.zeros((1, 1, 1, D))
+        q[0, 0, 0, 0] = 800.0
+        v = _rand((1, 1, Skv, D), 5)
+        o = impl(q, k, v, 0.125, False)  # logit gap 100: the other keys weigh e^-100
+        worst = max(worst, float(np.max(np.abs(o[0, 0, 0] - v[0, 0, jstar]))))
+    return worst
+
+
+def dev_single_key(impl):
+    """Sq = Skv = 1: the softmax has one entry, so O = v_0 whatever q, k and the scale are."""
+    q, k, v = _inputs(3, 4, 2, 1, 1, 8, 31)
+    worst = 0.0
+    for causal in (False, True):
+        o = impl(q * 50, k, v, 3.0, causal)
+        worst = max(worst, float(np.max(np.abs(o - np.repeat(v, 2, axis=1)))))
+    return worst
+
+
+def dev_sdpa(impl):
+    worst = 0.0
+    for n, (B, Hq, Hkv, Sq, Skv, D) in enumerate(RNG_SHAPES):
+        q, k, v = _inputs(B, Hq, Hkv, Sq, Skv, D, 40 + n)
+        for causal in (False, True):
+            o = impl(q, k, v, 0.35, causal)
+            ref = _sdpa64(q, k, v, 0.35, causal)
+            vis = _visible_count(Sq, Skv, causal) > 0  # SDPA gives NaN on empty rows
+            worst = max(worst, float(np.max(np.abs(o[:, :, vis] - ref[:, :, vis]))))
+    return worst
+
+
+def dev_bruteforce(impl):
+    worst = 0.0
+    for n, (B, Hq, Hkv, Sq, Skv, D) in enumerate([(1, 2, 1, 3, 4, 2), (1, 2, 2, 4, 3, 3),
+                                                   (2, 1, 1, 2, 5, 4)]):
+        q, k, v = _inputs(B, Hq, Hkv, Sq, Skv, D, 50 + n)
+        for causal in (False, True):
+            o = impl(q, k, v, 0.9, causal)
+            ref = np.array(oracle.attention_bruteforce(q.tolist(), k.tolist(), v.tolist(),
+                                                        0.9, causal))
+            worst = max(worst, float(np.max(np.abs(o - ref))))
+    return worst
+
+
+ALL_PINS = [dev_golden, dev_constant_v, dev_uniform_logits, dev_one_hot, dev_single_key,
+            dev_sdpa, dev_bruteforce]
+
+
+def _oracle_impl(q, k, v, scale, causal):
+    return oracle.attention_ref(q, k, v, scale, causal)
+
+
+@pytest.mark.parametrize("pin", ALL_PINS, ids=lambda f: f.__name__)
+def test_oracle_pins(pin):
+    assert pin(_oracle_impl) <= 1e-12
+
+
+@pytest.mark.parametrize("pin", [dev_golden, dev_constant_v, dev_uniform_logits, dev_one_hot,
+                                 dev_single_key], ids=lambda f: f.__name__)
+def test_bruteforce_pins(pin):
+    """The brute force is itself pinned by the closed forms (it is a second formulation)."""
+
+    def brute(q, k, v, scale, causal):
+        return np.array(oracle.attention_bruteforce(np.asarray(q).tolist(), np.asarray(k).tolist(),
+                                                    np.asarray(v).tolist(), scale, causal))
+
+    assert pin(brute) <= 1e-12
+
+
+def test_golden_combine_cases():
+    cases = json.load(open(GOLDEN))["combine"]
+    consts = {"ln2": math.log(2.0), "-inf": -math.inf}
+
+    def val(x):
+        if isinstance(x, list):
+            return [val(y) for y in x]
+        return consts[x] if isinstance(x, str) else float(x)
+
+    for c in cases:
+        o = oracle.combine_ref(np.array(val(c["m"])), np.array(val(c["l"])),
+                               np.array(val(c["acc"])))
+        np.testing.assert_allclose(o, np.array(val(c["o"])), rtol=0, atol=1e-14)
+
+
+# ---------------------------------------------------------------------------
+# Invariants
+# ---------------------------------------------------------------------------
+
+
+def test_softmax_rows_sum_to_one():
+    q, k, _ = _inputs(2, 4, 2, 6, 11, 8, 60)
+    for causal in (False, True):
+        o = oracle.attention_ref(q, k, np.ones((2, 2, 11, 8)), 0.5, causal)
+        np.testing.assert_allclose(o, 1.0, rtol=0, atol=1e-14)
+
+
+def test_key_permutation_invariance_noncausal():
+    q, k, v = _inputs(1, 4, 2, 5, 17, 8, 61)
+    perm = np.random.default_rng(0).permutation(17)
+    a = oracle.attention_ref(q, k, v, 0.4, False)
+    b = oracle.attention_ref(q, k[:, :, perm], v[:, :, perm], 0.4, False)
+    np.testing.assert_allclose(a, b, rtol=0, atol=1e-13)
+
+
+def test_future_keys_do_not_matter_causal():
+    Sq = Skv = 9
+    q, k, v = _inputs(1, 2, 1, Sq, Skv, 8, 62)
+    a = oracle.attention_ref(q, k, v, 0.4, True)
+    k2, v2 = k.copy(), v.copy()
+    k2[:, :, 5:] += 7.0
+    v2[:, :, 5:] -= 3.0
+    b = oracle.attention_ref(q, k2, v2, 0.4, True)
+    np.testing.assert_allclose(a[:, :, :5], b[:, :, :5], rtol=0, atol=1e-14)
+    assert np.max(np.abs(a[:, :, 5:] - b[:, :, 5:])) > 1e-3
+
+
+def test_decode_row_equals_last_prefill_row():
+    q, k, v = _inputs(1, 4, 2, 6, 6, 8, 63)
+    full = oracle.attention_ref(q, k, v, 0.3, True)
+    last = oracle.attention_ref(q[:, :, -1:], k, v, 0.3, True)
+    np.testing.assert_allclose(full[:, :, -1:], last, rtol=0, atol=1e-14)
+    # a chunk of the last 3 queries with the bottom-right mask equals the prefill rows
+    chunk = oracle.attention_ref(q[:, :, -3:], k, v, 0.3, True)
+    np.testing.assert_allclose(full[:, :, -3:], chunk, rtol=0, atol=1e-14)
+
+
+def test_gqa_equals_mha_on_repeated_kv():
+    q, k, v = _inputs(2, 8, 2, 5, 13, 8, 64)
+    for causal in (False, True):
+        a = oracle.attention_ref(q, k, v, 0.6, causal)
+        b = oracle.attention_ref(q, np.repeat(k, 4, axis=1), np.repeat(v, 4, axis=1), 0.6, causal)
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-15)
+
+
+def test_shift_of_keys_along_fixed_direction():
+    """k_j += u for every j adds q_i.u to a whole score row, which the softmax ignores."""
+    q, k, v = _inputs(1, 2, 2, 4, 10, 8, 65)
+    u = _rand((1, 2, 1, 8), 66)
+    for causal in (False, True):
+        a = oracle.attention_ref(q, k, v, 0.5, causal)
+        b = oracle.attention_ref(q, k + u, v, 0.5, causal)
+        np.testing.assert_allclose(a, b, rtol=0, atol=1e-12)
+
+
+def test_m0_m1_m2_agree():
+    for n, (B, Hq, Hkv, Sq, Skv, D) in enumerate(RNG_SHAPES):
+        q, k, v = _inputs(B, Hq, Hkv, Sq, Skv, D, 70 + n)
+        for causal in (False, True):
+            ref = oracle.attention_ref(q, k, v, 0.45, causal)
+            for tile in (1, 3, 4, Skv + 5):
+                np.testing.assert_allclose(
+                    oracle.m1_dependent_reductions(q, k, v, 0.45, causal, tile), ref,
+                    rtol=0, atol=1e-12)
+                np.testing.assert_allclose(
+                    oracle.m2_tiled_rolling(q, k, v, 0.45, causal, tile), ref,
+                    rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("T", [1, 2, 3, 5, 8, 64])
+def test_split_equals_unsplit(T):
+    for n, (B, Hq, Hkv, Sq, Skv, D) in enumerate(RNG_SHAPES):
+        q, k, v = _inputs(B, Hq, Hkv, Sq, Skv, D, 80 + n)
+        for causal in (False, True):
+            ref = oracle.attention_ref(q, k, v, 0.55, causal)
+            o = oracle.attention_splitkv_ref(q, k, v, 0.55, causal, T)
+            np.testing.assert_allclose(o, ref, rtol=0, atol=1e-12)
+
+
+def test_split_partials_layout_and_empty_identity():
+    """Causal early rows see no key of the late partitions: those slots are (-inf, 0, 0)."""
+    q, k, v = _inputs(1, 2, 1, 4, 12, 4, 90)
+    m, l, acc = oracle.splitkv_partials_ref(q, k, v, 0.5, True, 4)
+    assert m.shape == (8, 3) and l.shape == (8, 3) and acc.shape == (8, 3, 4)
+    # offset = 8: query i sees keys 0..8+i; query 0 sees only key 8 of partition 2
+    for hq in range(2):
+        r = hq * 4
+        assert np.isfinite(m[r]).all()
+        np.testing.assert_allclose(l[r, 2], 1.0, rtol=0, atol=0)
+        np.testing.assert_allclose(acc[r, 2], v[0, 0, 8], rtol=0, atol=0)
+    q2, k2, v2 = _inputs(1, 1, 1, 6, 4, 4, 91)
+    m2, l2, acc2 = oracle.splitkv_partials_ref(q2, k2, v2, 0.5, True, 2)
+    # offset = -2: query 0 and 1 see nothing; query 2 sees key 0 only
+    assert np.isneginf(m2[0]).all() and (l2[0] == 0).all() and (acc2[0] == 0).all()
+    assert np.isneginf(m2[2, 1]) and l2[2, 1] == 0
+    np.testing.assert_allclose(oracle.combine_ref(m2, l2, acc2)[:2], 0.0, rtol=0, atol=0)
+
+
+def test_partial_state_of_single_range_is_reference():
+    q, k, v = _inputs(1, 3, 3, 4, 9, 8, 92)
+    m, l, acc = oracle.splitkv_partials_ref(q, k, v, 0.5, False, 9)
+    ref = oracle.attention_ref(q, k, v, 0.5, False).reshape(12, 8)
+    np.testing.assert_allclose(acc[:, 0] / l[:, 0][:, None], ref, rtol=0, atol=1e-13)
+    s = np.einsum("bhqd,bhkd->bhqk", q, k).reshape(12, 9) * 0.5
+    np.testing.assert_allclose(m[:, 0], s.max(axis=1), rtol=0, atol=1e-14)
+
+
+def test_repair_identities():
+    """h(c, s, s') = c exp(s - s'): it moves a contribution g(y, s) = exp(x - s) y to the new
+    state s' and distributes over the sum reducer (section 4.2)."""
+    rng = np.random.default_rng(3)
+    x, y = rng.standard_normal(7), rng.standard_normal((7, 3))
+    s, s2 = 0.3, 1.7
+
+    def g(xx, yy, st):
+        return np.exp(xx - st)[:, None] * yy
+
+    def h(c, st, st2):
+        return c * np.exp(st - st2)
+
+    np.testing.assert_allclose(h(g(x, y, s), s, s2), g(x, y, s2), rtol=1e-14, atol=0)
+    a, b = g(x[:3], y[:3], s).sum(0), g(x[3:], y[3:], s).sum(0)
+    np.testing.assert_allclose(h(a + b, s, s2), h(a, s, s2) + h(b, s, s2), rtol=1e-14, atol=1e-15)
+
+
+def test_rolling_reducer_from_identity_matches_partial_state():
+    rng = np.random.default_rng(4)
+    scaled = rng.standard_normal((5, 11))
+    scaled[1, :] = -np.inf  # a row with nothing visible
+    scaled[2, :6] = -np.inf  # a row whose first tile is fully masked
+    vt = rng.standard_normal((11, 4))
+    state = (np.full(5, -np.inf), np.zeros(5), np.zeros((5, 4)))
+    for s, e in [(0, 6), (6, 7), (7, 11)]:
+        t = scaled[:, s:e]
+        state = oracle.rolling_update(state, t.max(axis=1), t, vt[s:e])
+    m, l, acc = oracle.partial_state(scaled, vt)
+    for a, b in zip(state, (m, l, acc)):
+        np.testing.assert_allclose(a, b, rtol=1e-14, atol=0)
+
+
+def test_combine_invariances():
+    rng = np.random.default_rng(5)
+    rows, P, D = 6, 5, 4
+    m = rng.standard_normal((rows, P)) * 3
+    l = rng.uniform(0.5, 9.0, (rows, P))
+    acc = rng.standard_normal((rows, P, D))
+    o = oracle.combine_ref(m, l, acc)
+    perm = rng.permutation(P)
+    np.testing.assert_allclose(oracle.combine_ref(m[:, perm], l[:, perm], acc[:, perm]), o,
+                               rtol=1e-13, atol=1e-14)
+    # (m + c, l e^-c, acc e^-c) describes the same partial state
+    c = 2.5
+    np.testing.assert_allclose(oracle.combine_ref(m + c, l * np.exp(-c), acc * np.exp(-c)), o,
+                               rtol=1e-12, atol=1e-13)
+    # appending identity partitions changes nothing
+    m2 = np.concatenate([m, np.full((rows, 2), -np.inf)], axis=1)
+    l2 = np.concatenate([l, np.zeros((rows, 2))], axis=1)
+    acc2 = np.concatenate([acc, np.zeros((rows, 2, D))], axis=1)
+    np.testing.assert_allclose(oracle.combine_ref(m2, l2, acc2), o, rtol=0, atol=0)
+    # one partition: o = acc / l
+    np.testing.assert_allclose(oracle.combine_ref(m[:, :1], l[:, :1], acc[:, :1]),
+                               acc[:, 0] / l[:, :1], rtol=1e-15, atol=0)
+    np.testing.assert_allclose(oracle.combine_error_scale(m[:, :1], l[:, :1], acc[:, :1]),
+                               np.abs(acc[:, 0]) / l[:, :1], rtol=1e-15, atol=0)
+
+
+def test_combine_of_fp32_partials_is_widened_exactly():
+    rng = np.random.default_rng(6)
+    m = (rng.standard_normal((3, 4)) * 2).astype(np.float32)
+    l = rng.uniform(1, 2, (3, 4)).astype(np.float32)
+    acc = rng.standard_normal((3, 4, 5)).astype(np.float32)
+    a = oracle.combine_ref(m, l, acc)
+    b = oracle.combine_ref(m.astype(np.float64), l.astype(np.float64), acc.astype(np.float64))
+    np.testing.assert_array_equal(a, b)
+
+
+def test_partition_bounds():
+    assert oracle.partition_bounds(10, 4) == [(0, 4), (4, 8), (8, 10)]
+    assert oracle.partition_bounds(8, 4) == [(0, 4), (4, 8)]
+    assert oracle.partition_bounds(3, 8) == [(0, 3)]
+    with pytest.raises(ValueError):
+        oracle.partition_bounds(3, 0)
+
+
+def test_oracle_imports_nothing_from_the_hip_path():
+    src = open(oa.__file__).read()
+    assert "paper_2609_12330_amd" not in src and "ctypes" not in src and "torch" not in src
+
+
+# ---------------------------------------------------------------------------
+# Mutation tests: each plausible mistake, planted in the oracle on the CPU, must
+# make at least one pin fail.
+# ---------------------------------------------------------------------------
+
+
+def _fails_some_pin(impl):
+    return any(pin(impl) > 1e-6 for pin in ALL_PINS)
+
+
+def test_mutant_scale_dropped():
+    assert _fails_some_pin(lambda q, k, v, s, c: oracle.attention_ref(q, k, v, 1.0, c))
+
+
+def test_mutant_scale_sign_flipped():
+    assert _fails_some_pin(lambda q, k, v, s, c: oracle.attention_ref(q, k, v, -s, c))
+
+
+def test_mutant_causal_top_left(monkeypatch):
+    monkeypatch.setattr(oa, "causal_visible",
+                        lambda Sq, Skv: np.arange(Skv)[None, :] <= np.arange(Sq)[:, None])
+    assert _fails_some_pin(_oracle_impl)
+
+
+def test_mutant_causal_off_by_one(monkeypatch):
+    monkeypatch.setattr(oa, "causal_visible",
+                        lambda Sq, Skv: np.arange(Skv)[None, :] < np.arange(Sq)[:, None] + Skv - Sq)
+    assert _fails_some_pin(_oracle_impl)
+
+
+def test_mutant_gqa_head_mapping_modulo():
+    """Query head hq reads kv head hq % Hkv instead of hq // G."""
+
+    def mutant(q, k, v, s, c):
+        Hq, Hkv = q.shape[1], k.shape[1]
+        G = Hq // Hkv
+        sigma = [(h % Hkv) * G + h // Hkv for h in range(Hq)]
+        q2 = np.empty_like(q)
+        q2[:, sigma] = q
+        return oracle.attention_ref(q2, k, v, s, c)[:, sigma]
+
+    assert _fails_some_pin(mutant)
+
+
+def test_mutant_keys_used_as_values():
+    assert _fails_some_pin(lambda q, k, v, s, c: oracle.attention_ref(q, k, k, s, c))
+
+
+def test_mutant_softmax_over_queries(monkeypatch):
+    def bad(scaled, vh):
+        mx = scaled.max(axis=0, initial=-np.inf)
+        w = np.where(np.isfinite(scaled), np.exp(scaled - np.where(np.isfinite(mx), mx, 0)), 0)
+        den = w.sum(axis=0)
+        return (w / np.where(den > 0, den, 1)) @ vh
+
+    monkeypatch.setattr(oa, "_softmax_rows_times_v", bad)
+    assert _fails_some_pin(_oracle_impl)
+
+
+def test_mutant_rolling_without_rescale(monkeypatch):
+    real = oa.rolling_update
+
+    def bad(state, block_max, scaled_tile, v_tile):
+        mx, sm, val = state
+        nm, ns, nv = real(state, block_max, scaled_tile, v_tile)
+        w = np.exp(scaled_tile - np.where(np.isfinite(nm), nm, 0)[:, None])
+        w = np.where(np.isfinite(scaled_tile), w, 0.0)
+        return nm, sm + w.sum(axis=1), val + w @ v_tile  # stale state not rescaled
+
+    monkeypatch.setattr(oa, "rolling_update", bad)
+    assert _fails_some_pin(lambda q, k, v, s, c: oracle.m2_tiled_rolling(q, k, v, s, c, 3))
+
+
+def test_mutant_combine_without_weights():
+    def bad_combine(m, l, acc):
+        L = l.sum(axis=1)
+        return np.where(L[:, None] > 0, acc.sum(axis=1) / np.where(L > 0, L, 1)[:, None], 0.0)
+
+    def mutant(q, k, v, s, c):
+        B, Hq, Sq, D = q.shape
+        m, l, acc = oracle.splitkv_partials_ref(q, k, v, s, c, 2)
+        return bad_combine(m, l, acc).reshape(B, Hq, Sq, D)
+
+    assert _fails_some_pin(mutant)
+    # and the real combine over the same partials passes every pin
+    assert not _fails_some_pin(lambda q, k, v, s, c: oracle.attention_splitkv_ref(q, k, v, s, c, 2))

@@ -1,0 +1,51 @@
+"""The seeded input generator: determinism, shapes, dtypes and the accounting figures."""
+
+import torch
+
+from paper_2609_12330_amd import workloads as wl
+
+
+def test_configs_shapes_and_accounting():
+    c = wl.CONFIG_BY_NAME
+    tiny = c["tiny_mha_b1_h4_s64_d64"]
+    assert (tiny.B, tiny.Hq, tiny.Hkv, tiny.Sq, tiny.Skv, tiny.D) == (1, 4, 4, 64, 64, 64)
+    assert tiny.flops() == 4_194_304 and tiny.algorithmic_bytes() == 163_840
+    dec = c["gqa_decode_b8_h32x8_kv4096_d128"]
+    assert dec.G == 4 and dec.partition_size == 256
+    assert dec.kv_bytes() == 134_217_728 and dec.algorithmic_bytes() == 134_414_336
+    assert dec.flops() == 536_870_912
+    pre = c["causal_gqa_prefill_b4_h32x8_s2048_d128"]
+    assert pre.visible_pairs() == 268_566_528 and pre.flops() == 137_506_062_336
+    assert pre.algorithmic_bytes() == 234_881_024
+    lng = c["long_decode_b1_h32x8_kv131072_d128"]
+    assert lng.Skv // lng.partition_size == 512 and lng.algorithmic_bytes() == 536_895_488
+    chk = c["chunked_decode_b16_h64x8_q8_kv8192_d128"]
+    assert chk.visible_pairs() == 67_080_192 and chk.flops() == 34_345_058_304
+    assert chk.algorithmic_bytes() == 543_162_368
+    for cfg in wl.CONFIGS:
+        assert abs(cfg.scale - cfg.D ** -0.5) < 1e-12
+
+
+def test_make_inputs_deterministic_bf16():
+    cfg = wl.CONFIG_BY_NAME["tiny_mha_b1_h4_s64_d64"]
+    a = wl.make_inputs(cfg, 7)
+    b = wl.make_inputs(cfg, 7)
+    c = wl.make_inputs(cfg, 8)
+    for x, y in zip(a, b):
+        assert x.dtype == torch.bfloat16 and torch.equal(x, y)
+    assert not torch.equal(a[0], c[0])
+    assert a[0].shape == (1, 4, 64, 64) and a[1].shape == (1, 4, 64, 64)
+
+
+def test_q_mult_doubles_exactly():
+    base = wl.make_shape_inputs(1, 4, 2, 1, 64, 128, seed=3)
+    dbl = wl.make_shape_inputs(1, 4, 2, 1, 64, 128, seed=3, q_mult=2.0)
+    assert torch.equal(dbl[0].float(), 2.0 * base[0].float())
+    assert torch.equal(dbl[1], base[1]) and torch.equal(dbl[2], base[2])
+
+
+def test_partials_generator_empty_slots():
+    m, l, acc = wl.make_partials(64, 9, 16, seed=1, empty_frac=0.3)
+    empty = torch.isneginf(m)
+    assert empty.any() and (~empty).any()
+    assert (l[empty] == 0).all() and (acc[empty] == 0).all()
