@@ -1,0 +1,261 @@
+#!/usr/bin/env python3
+"""Throughput of the split-KV attention hot path on one MI355X.
+
+One step = one pass of the whole path over one batch: the split-KV producer
+(q.k^T, scale, running max, exp, running sum, p.v over every key partition,
+stored partial states) followed by the combine kernel that merges the states
+into o. The default workload is grouped-query decode, B=8, Hq=32, Hkv=8,
+Sq=1, Skv=4096, D=128, 256-key partitions; the metric is KV bytes read per
+second over the whole step. K/V inputs rotate over enough buffer sets that
+no step finds its K/V in the 256 MB last-level cache left by the step before.
+
+Prints one JSON line. `--config` selects another workload (the causal prefill
+is reported in TFLOP/s through ef_attention_fwd).
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "attention TFLOP/s (prefill) and KV-read GB/s (decode), % of MI355X roofline"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+MALL_BYTES = 256 << 20
+PROFILE_DIR = os.path.join(ROOT, "profiles")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--config", default="gqa_decode_b8_h32x8_kv4096_d128")
+    ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="CPU work budget of the oracle baseline (0 disables it)")
+    return ap.parse_args()
+
+
+def source_hash(*names):
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(ROOT, "paper_2609_12330_amd", "csrc", n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def load_traffic(kernel_key, src_hash, units_per_launch):
+    """HBM bytes per launch from committed rocprofv3 counter runs, if they match this source."""
+    path = os.path.join(PROFILE_DIR, f"{kernel_key}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        t = json.load(f)
+    if t.get("source_hash") != src_hash:
+        return None
+    return float(t["hbm_bytes_per_launch"])
+
+
+def cpu_baseline(cfg, q, k, v, budget_s, unit_fn):
+    """Time the fp64 oracle as it stands on this host over repeated passes of the workload."""
+    import numpy as np
+
+    import oracle
+    from paper_2609_12330_amd import workloads as wl
+
+    threads = None
+    try:
+        import threadpoolctl
+
+        info = threadpoolctl.threadpool_info()
+        threads = max((i.get("num_threads") or 0) for i in info) if info else None
+    except Exception:
+        pass
+    Q, K, V = wl.to_f64(q), wl.to_f64(k), wl.to_f64(v)
+    # Bound the sample: whole kv-head groups of the workload, enough for ~budget_s of work.
+    B = cfg.B
+    t0 = time.perf_counter()
+    oracle.attention_ref(Q[:1], K[:1], V[:1], cfg.scale, cfg.causal)
+    one = max(time.perf_counter() - t0, 1e-6)
+    reps = max(1, int(budget_s / one))
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        oracle.attention_ref(Q[:1], K[:1], V[:1], cfg.scale, cfg.causal)
+    dt = time.perf_counter() - t0
+    value = unit_fn(reps / B) / dt  # the work of `reps` batch rows of the workload per second
+    return {
+        "value": round(value, 4),
+        "cores": threads or os.cpu_count(),
+        "kind": "oracle",
+        "sample": f"{reps} passes of batch row 0 of the workload (Hq={cfg.Hq}, Hkv={cfg.Hkv}, "
+                  f"Sq={cfg.Sq}, Skv={cfg.Skv}, D={cfg.D}) through the fp64 numpy oracle, "
+                  f"inputs widened to fp64 once outside the timing; {dt:.1f} s",
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build runs on a single MI355X and has no "
+              "multi-GPU path (run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_12330_amd import ef_attention as ef
+    from paper_2609_12330_amd import workloads as wl
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    ef.library()  # fails loudly when the HIP library is missing
+    cfg = wl.CONFIG_BY_NAME[args.config]
+    seed = args.seed if args.seed is not None else wl.DEFAULT_SEED[cfg.name]
+    dev = torch.device("cuda:0")
+    decode = cfg.Sq * cfg.G <= 64 and cfg.Skv >= 1024 and not (cfg.Sq == cfg.Skv)
+
+    # Buffer sets: the K/V of consecutive steps never share a 256 MB cache footprint.
+    kv = cfg.kv_bytes()
+    nbuf = 1 if kv == 0 else max(2, math.ceil(2.5 * MALL_BYTES / kv))
+    nbuf = min(nbuf, 8)
+    q_cpu, k_cpu, v_cpu = wl.make_inputs(cfg, seed)
+    sets = []
+    for i in range(nbuf):
+        if i == 0:
+            q, k, v = q_cpu, k_cpu, v_cpu
+        else:
+            q, k, v = wl.make_inputs(cfg, seed + 1000 * i)
+        sets.append((q.to(dev), k.to(dev), v.to(dev)))
+    o = torch.empty(cfg.B, cfg.Hq, cfg.Sq, cfg.D, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    sh = stream.cuda_stream
+    B, Hq, Hkv, Sq, Skv, D = cfg.B, cfg.Hq, cfg.Hkv, cfg.Sq, cfg.Skv, cfg.D
+
+    if decode:
+        T = ef.splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, cfg.partition_size)
+        P = -(-Skv // T)
+        ws = ef.make_workspace(sets[0][0], sets[0][1], T)
+        wsb = ws.numel()
+        m, l, acc = ef.workspace_views(ws, B, Hq, Sq, Skv, D, T)
+        rows = B * Hq * Sq
+
+        def step(i, ev=None):
+            q, k, v = sets[i % nbuf]
+            if ev is not None:
+                ev[0].record(stream)
+            st = ef.ef_attention_splitkv_partials(q.data_ptr(), k.data_ptr(), v.data_ptr(), B, Hq,
+                                                  Hkv, Sq, Skv, D, cfg.scale, cfg.causal, T,
+                                                  ws.data_ptr(), wsb, sh)
+            if ev is not None:
+                ev[1].record(stream)
+            st |= ef.ef_attention_combine(m.data_ptr(), l.data_ptr(), acc.data_ptr(), o.data_ptr(),
+                                          rows, P, D, sh)
+            if ev is not None:
+                ev[2].record(stream)
+            if st:
+                raise RuntimeError(f"library error {st}")
+    else:
+        T, P = Skv, 1
+
+        def step(i, ev=None):
+            q, k, v = sets[i % nbuf]
+            if ev is not None:
+                ev[0].record(stream)
+            st = ef.ef_attention_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B, Hq,
+                                     Hkv, Sq, Skv, D, cfg.scale, cfg.causal, sh)
+            if ev is not None:
+                ev[1].record(stream)
+                ev[2].record(stream)
+            if st:
+                raise RuntimeError(f"library error {st}")
+
+    for i in range(args.warmup):
+        step(i)
+    torch.cuda.synchronize()
+    print(f"[bench] {cfg.name}: warmup done ({args.warmup} steps, {nbuf} buffer sets)",
+          file=sys.stderr, flush=True)
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(args.warmup + i, evs[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms_step = wall * 1e3 / args.steps
+    prod_ms = [e[0].elapsed_time(e[1]) for e in evs]
+    comb_ms = [e[1].elapsed_time(e[2]) for e in evs]
+    prod_avg = sum(prod_ms) / len(prod_ms)
+    comb_avg = sum(comb_ms) / len(comb_ms)
+    print(f"[bench] timed {args.steps} steps: {ms_step * 1e3:.2f} us/step, producer "
+          f"{prod_avg * 1e3:.2f} us, combine {comb_avg * 1e3:.2f} us", file=sys.stderr, flush=True)
+
+    q_bytes = B * Hq * Sq * D * 2
+    if decode:
+        # Producer: algorithmic bytes = bf16 q + K + V read once (512 B per key per kv head).
+        kernel = "decode_split" if cfg.Sq * cfg.G <= 8 else "attn_mfma_split"
+        src = source_hash("decode_split.hip" if kernel == "decode_split" else "attn_mfma.hip",
+                          "ef_device.hpp")
+        alg = kv + q_bytes
+        achieved = alg / (prod_avg * 1e-3) / 1e9
+        traffic = load_traffic(f"{kernel}_{cfg.name}", src, 1)
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": kernel, "algorithmic_bytes_per_launch": alg}
+        value = kv / (ms_step * 1e-3) / 1e9
+        unit = "GB/s"
+        unit_fn = lambda batches: kv * batches / 1e9  # noqa: E731
+    else:
+        kernel = "attn_mfma"
+        src = source_hash("attn_mfma.hip", "ef_device.hpp")
+        flops = cfg.flops()
+        achieved = flops / (prod_avg * 1e-3) / 1e12
+        traffic = load_traffic(f"{kernel}_{cfg.name}", src, 1)
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
+                "traffic": traffic, "kernel": kernel, "algorithmic_flops_per_launch": flops}
+        value = flops / (ms_step * 1e-3) / 1e12
+        unit = "TFLOP/s"
+        unit_fn = lambda batches: flops * batches / 1e12  # noqa: E731
+
+    cpu = None
+    if args.cpu_seconds > 0:
+        print("[bench] timing the fp64 oracle on the host", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(cfg, q_cpu, k_cpu, v_cpu, args.cpu_seconds, unit_fn)
+        cpu["unit"] = unit
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": unit,
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded i.i.d. N(0,1) bf16 q/k/v)",
+        "config": {"workload": cfg.name, "B": B, "Hq": Hq, "Hkv": Hkv, "Sq": Sq, "Skv": Skv,
+                   "D": D, "causal": bool(cfg.causal), "partition_size": T if decode else None,
+                   "partitions": P, "kv_buffer_sets": nbuf, "parallelism": "single GPU"},
+        "roofline": roof,
+        "cpu_baseline": cpu,
+        "kernel_us": {"producer": round(prod_avg * 1e3, 3), "combine": round(comb_avg * 1e3, 3)},
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,162 @@
+/*
+ * ef_attention.h - C ABI of the MI355X (gfx950) fused attention library.
+ *
+ * The library computes the fused attention program of EquiForge (arXiv
+ * 2609.12330): for every batch b and query head hq, with kv head
+ * hk = hq / (Hq / Hkv) (replication by index, section 3.1 "Replicate"),
+ *
+ *     s_ij = scale * <q_i, k_j>,   O_i = sum_j exp(s_ij - m_i) v_j / sum_j exp(s_ij - m_i),
+ *     m_i  = max_j s_ij,
+ *
+ * which is form M0 of figure "attention-rewrites" (section 3). The kernels
+ * evaluate it as form M2 of the same figure: the key axis is cut into tiles
+ * and a rolling (max, sum, value) reducer is carried over them (section 4.2,
+ * repair fusion with h(c, s, s') = c * exp(s - s')). The split-KV entry point
+ * additionally stores one reduced state per key partition and combines them
+ * in a second kernel (section 3.3 "Collection"; section 4.4 storage rule).
+ *
+ * Conventions shared by every entry point
+ *   - Tensors are dense and row-major with the head dimension innermost:
+ *       q  [B][Hq ][Sq ][D] bf16      k, v [B][Hkv][Skv][D] bf16
+ *       o  [B][Hq ][Sq ][D] fp32
+ *     bf16 is the IEEE binary32 upper half (1-8-7). All pointers are DEVICE
+ *     pointers, 16-byte aligned; the caller owns every buffer and keeps it
+ *     alive until the stream has passed the call. The library allocates
+ *     nothing and keeps no state between calls; calls are thread-safe.
+ *   - D must be 64 or 128. Hq and Hkv must be >= 1 with Hq % Hkv == 0.
+ *     B, Sq and Skv may be 0: with B*Hq*Sq == 0 nothing is written, with
+ *     Skv == 0 every output row is 0. Per head, S*D must stay below 2^31.
+ *   - causal != 0 applies a bottom-right aligned mask: key j is visible to
+ *     query i iff j <= i + (Skv - Sq). A query row that sees no key gets 0.
+ *   - scale multiplies the fp32-accumulated q.k products; it must be finite.
+ *   - Every call validates its arguments on the host, synchronously, before
+ *     anything is enqueued. On an error nothing is launched and no buffer is
+ *     written. After validation the work is enqueued on `stream` (a
+ *     hipStream_t; NULL is the default stream) and the call returns without
+ *     waiting; a launch failure reported by HIP returns EF_ERR_HIP.
+ *   - Results are deterministic: the same inputs give bitwise equal outputs.
+ */
+#ifndef EF_ATTENTION_H
+#define EF_ATTENTION_H
+
+#include <stddef.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define EF_ABI_VERSION 1
+
+typedef enum {
+  EF_OK = 0,
+  EF_ERR_NULL_POINTER = 1,         /* a required pointer is NULL */
+  EF_ERR_INVALID_SHAPE = 2,        /* a negative size, Hq or Hkv < 1, or a head too large */
+  EF_ERR_GQA_RATIO = 3,            /* Hq is not a multiple of Hkv */
+  EF_ERR_UNSUPPORTED_HEAD_DIM = 4, /* D is not 64 or 128 */
+  EF_ERR_MISALIGNED = 5,           /* a pointer is not 16-byte aligned */
+  EF_ERR_INVALID_PARTITION = 6,    /* partition_size is not 0 or a positive multiple of 64 */
+  EF_ERR_WORKSPACE_TOO_SMALL = 7,  /* workspace is NULL or smaller than required */
+  EF_ERR_INVALID_SCALE = 8,        /* scale is NaN or infinite */
+  EF_ERR_HIP = 9                   /* HIP reported an error when the work was enqueued */
+} ef_status;
+
+/* Version of this ABI (EF_ABI_VERSION). */
+int ef_abi_version(void);
+
+/* Static, NUL-terminated description of a status code; never NULL. */
+const char* ef_status_string(int status);
+
+/*
+ * Single-pass attention: form M2 of figure "attention-rewrites". The query
+ * rows that share a kv head are tiled along the query axis (grid axis m), each
+ * workgroup carries the rolling reducer over all key tiles it can see and
+ * writes O = value / sum once at the end (section 6.1: output-tile axes map
+ * to the grid, reduction axes to an in-workgroup loop).
+ *   q, k, v, o : device buffers in the layouts above.
+ *   B, Hq, Hkv, Sq, Skv, D, scale, causal : as above.
+ *   stream     : hipStream_t or NULL.
+ */
+ef_status ef_attention_fwd(const void* q, const void* k, const void* v, float* o,
+                           int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                           float scale, int causal, void* stream);
+
+/*
+ * Partition size, in keys, that ef_attention_splitkv uses for these sizes:
+ * `partition_size` itself when it is positive, else the library's choice
+ * (a multiple of 64 that spreads the B*Hkv*P workgroups over the chip).
+ * Returns 0 when the arguments are invalid.
+ */
+int ef_attention_splitkv_partition_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                        int partition_size);
+
+/*
+ * Bytes of workspace ef_attention_splitkv needs for these sizes (0 when the
+ * arguments are invalid or nothing is computed). With rows = B*Hq*Sq,
+ * P = ceil(Skv / T) and T the resolved partition size, the workspace holds
+ *     m   [rows][P]    fp32 at byte 0
+ *     l   [rows][P]    fp32 at byte  A = round_up(rows*P*4, 256)
+ *     acc [rows][P][D] fp32 at byte 2*A
+ * with row = (b*Hq + hq)*Sq + sq: a reference point m for the scaled scores
+ * s of the row's visible keys in partition p (natural-log units; at most the
+ * partition maximum and within 8*ln(2) of it), l = sum exp(s - m) and
+ * acc = sum exp(s - m) * v. (m, l, acc) and (m', l*e^(m-m'), acc*e^(m-m'))
+ * describe the same state. A partition with no visible key holds the reducer
+ * identity (-inf, 0, 0).
+ */
+size_t ef_attention_splitkv_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                           int partition_size);
+
+/*
+ * Split-KV attention for decode-shaped problems (few query rows per kv head,
+ * long key axis). The key axis is cut into P partitions of T keys; one
+ * workgroup per (partition, kv head, batch) reads its K/V slice once, serves
+ * all Hq/Hkv * Sq query rows of that kv head, and stores the reduced state
+ * (m, l, acc) of every row in the workspace (the Collection of section 3.3
+ * and the storage rule of section 4.4). A second kernel combines the P states
+ * of each row with the same reducer and writes o (section 4.1, reduction
+ * refinement along K; section 4.2, repair fusion).
+ *   partition_size   : T in keys; 0 lets the library choose; otherwise a
+ *                      positive multiple of 64.
+ *   workspace        : device buffer of at least
+ *                      ef_attention_splitkv_workspace_size(...) bytes,
+ *                      16-byte aligned; on return (stream-ordered) it holds
+ *                      the partial states in the layout documented there.
+ *   workspace_bytes  : its size in bytes.
+ * Other arguments as for ef_attention_fwd.
+ */
+ef_status ef_attention_splitkv(const void* q, const void* k, const void* v, float* o,
+                               int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                               float scale, int causal, int partition_size,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The producer step of ef_attention_splitkv alone: the same validation and
+ * the same kernels, writing only the partial states into the workspace
+ * (layout of ef_attention_splitkv_workspace_size). Combining them with
+ * ef_attention_combine gives ef_attention_splitkv's output; partial states of
+ * disjoint key ranges (e.g. computed on different devices, each over its own
+ * slice of the key axis) may be concatenated along P before the combine,
+ * since the combine applies the same reducer to any set of stored states.
+ */
+ef_status ef_attention_splitkv_partials(const void* q, const void* k, const void* v,
+                                        int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                        float scale, int causal, int partition_size,
+                                        void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The combine step alone, over caller-provided fp32 partial states:
+ *   m [rows][P], l [rows][P], acc [rows][P][D] (device, 16-byte aligned),
+ *   o [rows][D] fp32 output.
+ * For each row: M = max_p m_p, w_p = exp(m_p - M) (0 where m_p = -inf),
+ * o = (sum_p w_p acc_p) / (sum_p w_p l_p), and o = 0 when M = -inf
+ * (section 4.2, the fused reducer applied to stored states).
+ * rows >= 0, P >= 1, D in {64, 128}.
+ */
+ef_status ef_attention_combine(const float* m, const float* l, const float* acc, float* o,
+                               int rows, int num_partitions, int D, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EF_ATTENTION_H */

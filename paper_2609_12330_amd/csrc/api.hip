@@ -1,0 +1,274 @@
+// Host side of the C ABI declared in include/ef_attention.h: argument
+// validation (synchronous, before anything is enqueued), kernel selection,
+// grid and workspace arithmetic.
+#include <cmath>
+#include <cstdint>
+
+#include "ef_attention.h"
+#include "ef_device.hpp"
+#include "ef_kernels.hpp"
+
+namespace {
+
+constexpr int kTileKeys = 64;        // key tile of the kernels; partitions are multiples of it
+constexpr int kDecodeMaxRows = 8;    // the VALU split producer serves G*Sq <= 8
+constexpr int kTargetBlocks = 1024;  // split producer workgroups the heuristic aims for
+constexpr int kMaxGridYZ = 65535;
+
+struct Shape {
+  int B, Hq, Hkv, Sq, Skv, D;
+  long long rows() const { return (long long)B * Hq * Sq; }
+};
+
+bool misaligned(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) != 0; }
+
+ef_status check_shape(const Shape& s) {
+  if (s.B < 0 || s.Sq < 0 || s.Skv < 0 || s.Hq < 1 || s.Hkv < 1) return EF_ERR_INVALID_SHAPE;
+  if (s.Hq % s.Hkv != 0) return EF_ERR_GQA_RATIO;
+  if (s.D != 64 && s.D != 128) return EF_ERR_UNSUPPORTED_HEAD_DIM;
+  // Per-head extents stay below 2^31 elements; batch*heads fits the grid.
+  if ((long long)s.Sq * s.D >= (1LL << 31) || (long long)s.Skv * s.D >= (1LL << 31))
+    return EF_ERR_INVALID_SHAPE;
+  if ((long long)s.B * s.Hkv > kMaxGridYZ || (long long)(s.Hq / s.Hkv) * s.Sq >= (1LL << 31))
+    return EF_ERR_INVALID_SHAPE;
+  return EF_OK;
+}
+
+ef_status check_io(const Shape& s, const void* q, const void* k, const void* v, const float* o,
+                   float scale) {
+  if (!std::isfinite(scale)) return EF_ERR_INVALID_SCALE;
+  if (s.rows() == 0) return EF_OK;
+  if (q == nullptr || o == nullptr) return EF_ERR_NULL_POINTER;
+  if (s.Skv > 0 && (k == nullptr || v == nullptr)) return EF_ERR_NULL_POINTER;
+  if (misaligned(q) || misaligned(o) || misaligned(k) || misaligned(v)) return EF_ERR_MISALIGNED;
+  return EF_OK;
+}
+
+int resolve_partition(const Shape& s, int partition_size) {
+  if (partition_size > 0) return partition_size;
+  if (s.Skv <= 0) return kTileKeys;
+  const long long kv_heads = (long long)s.B * s.Hkv;
+  long long parts = (kTargetBlocks + kv_heads - 1) / kv_heads;
+  if (parts < 1) parts = 1;
+  long long t = (s.Skv + parts - 1) / parts;
+  t = (t + kTileKeys - 1) / kTileKeys * kTileKeys;
+  if (t < 256) t = 256;  // keep the stored state small against the K/V bytes read
+  if (t > s.Skv) t = (s.Skv + kTileKeys - 1) / kTileKeys * kTileKeys;
+  return (int)t;
+}
+
+struct WsLayout {
+  size_t m_off, l_off, acc_off, bytes;
+};
+
+WsLayout ws_layout(long long rows, long long P, int D) {
+  WsLayout w;
+  const size_t a = ef::ws_align256((size_t)(rows * P) * sizeof(float));
+  w.m_off = 0;
+  w.l_off = a;
+  w.acc_off = 2 * a;
+  w.bytes = 2 * a + (size_t)(rows * P) * (size_t)D * sizeof(float);
+  return w;
+}
+
+ef_status from_hip(hipError_t e) { return e == hipSuccess ? EF_OK : EF_ERR_HIP; }
+
+ef_status launch_mfma(const Shape& s, const void* q, const void* k, const void* v, float* o,
+                      float* ws_m, float* ws_l, float* ws_acc, int T, int P, float scale,
+                      int causal, hipStream_t stream) {
+  ef::MfmaParams a{};
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.o = o;
+  a.ws_m = ws_m;
+  a.ws_l = ws_l;
+  a.ws_acc = ws_acc;
+  a.B = s.B; a.Hq = s.Hq; a.Hkv = s.Hkv; a.Sq = s.Sq; a.Skv = s.Skv; a.D = s.D;
+  a.G = s.Hq / s.Hkv;
+  a.R = a.G * s.Sq;
+  a.T = T;
+  a.P = P;
+  const int bm = ef::mfma_rows_per_block(a.R);
+  a.mtiles = (a.R + bm - 1) / bm;
+  a.c_abs = std::fabs(scale) * ef::kLog2e;
+  a.causal = causal ? 1 : 0;
+  return from_hip(ef::launch_mfma_attention(a, scale < 0.f, stream));
+}
+
+}  // namespace
+
+extern "C" {
+
+int ef_abi_version(void) { return EF_ABI_VERSION; }
+
+const char* ef_status_string(int status) {
+  switch (status) {
+    case EF_OK: return "ok";
+    case EF_ERR_NULL_POINTER: return "a required pointer is NULL";
+    case EF_ERR_INVALID_SHAPE: return "invalid shape (negative size, Hq or Hkv < 1, or too large)";
+    case EF_ERR_GQA_RATIO: return "Hq is not a multiple of Hkv";
+    case EF_ERR_UNSUPPORTED_HEAD_DIM: return "head dimension must be 64 or 128";
+    case EF_ERR_MISALIGNED: return "a pointer is not 16-byte aligned";
+    case EF_ERR_INVALID_PARTITION: return "partition_size must be 0 or a positive multiple of 64";
+    case EF_ERR_WORKSPACE_TOO_SMALL: return "workspace is NULL or too small";
+    case EF_ERR_INVALID_SCALE: return "scale is not finite";
+    case EF_ERR_HIP: return "HIP error while enqueueing work";
+    default: return "unknown status";
+  }
+}
+
+ef_status ef_attention_fwd(const void* q, const void* k, const void* v, float* o, int B, int Hq,
+                           int Hkv, int Sq, int Skv, int D, float scale, int causal,
+                           void* stream) {
+  const Shape s{B, Hq, Hkv, Sq, Skv, D};
+  ef_status st = check_shape(s);
+  if (st != EF_OK) return st;
+  st = check_io(s, q, k, v, o, scale);
+  if (st != EF_OK) return st;
+  if (s.rows() == 0) return EF_OK;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (Skv == 0) return from_hip(ef::launch_zero_fill(o, (size_t)s.rows() * D, hs));
+  return launch_mfma(s, q, k, v, o, nullptr, nullptr, nullptr, Skv, 1, scale, causal, hs);
+}
+
+int ef_attention_splitkv_partition_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                        int partition_size) {
+  const Shape s{B, Hq, Hkv, Sq, Skv, D};
+  if (check_shape(s) != EF_OK) return 0;
+  if (partition_size < 0 || partition_size % kTileKeys != 0) return 0;
+  return resolve_partition(s, partition_size);
+}
+
+size_t ef_attention_splitkv_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                           int partition_size) {
+  const Shape s{B, Hq, Hkv, Sq, Skv, D};
+  if (check_shape(s) != EF_OK) return 0;
+  if (partition_size < 0 || partition_size % kTileKeys != 0) return 0;
+  if (s.rows() == 0 || Skv == 0) return 0;
+  const int T = resolve_partition(s, partition_size);
+  const long long P = (Skv + (long long)T - 1) / T;
+  return ws_layout(s.rows(), P, D).bytes;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Validation shared by the split-KV entry points; on success fills the
+// partition count and the workspace pointers.
+ef_status split_prepare(const Shape& s, const void* q, const void* k, const void* v,
+                        const float* o, float scale, int partition_size, void* workspace,
+                        size_t workspace_bytes, int* T_out, int* P_out, float** ws_m,
+                        float** ws_l, float** ws_acc) {
+  ef_status st = check_shape(s);
+  if (st != EF_OK) return st;
+  if (partition_size < 0 || partition_size % kTileKeys != 0) return EF_ERR_INVALID_PARTITION;
+  st = check_io(s, q, k, v, o, scale);
+  if (st != EF_OK) return st;
+  *T_out = 0;
+  *P_out = 0;
+  if (s.rows() == 0 || s.Skv == 0) return EF_OK;
+  const int T = resolve_partition(s, partition_size);
+  const long long P = (s.Skv + (long long)T - 1) / T;
+  if (P > kMaxGridYZ) return EF_ERR_INVALID_PARTITION;
+  const WsLayout w = ws_layout(s.rows(), P, s.D);
+  if (workspace == nullptr || workspace_bytes < w.bytes) return EF_ERR_WORKSPACE_TOO_SMALL;
+  if (misaligned(workspace)) return EF_ERR_MISALIGNED;
+  char* ws = static_cast<char*>(workspace);
+  *ws_m = reinterpret_cast<float*>(ws + w.m_off);
+  *ws_l = reinterpret_cast<float*>(ws + w.l_off);
+  *ws_acc = reinterpret_cast<float*>(ws + w.acc_off);
+  *T_out = T;
+  *P_out = (int)P;
+  return EF_OK;
+}
+
+ef_status split_produce(const Shape& s, const void* q, const void* k, const void* v, float scale,
+                        int causal, int T, int P, float* ws_m, float* ws_l, float* ws_acc,
+                        hipStream_t hs) {
+  const int G = s.Hq / s.Hkv;
+  const int R = G * s.Sq;
+  if (R <= kDecodeMaxRows) {
+    ef::DecodeParams a{};
+    a.q = static_cast<const uint16_t*>(q);
+    a.k = static_cast<const uint16_t*>(k);
+    a.v = static_cast<const uint16_t*>(v);
+    a.ws_m = ws_m;
+    a.ws_l = ws_l;
+    a.ws_acc = ws_acc;
+    a.B = s.B; a.Hq = s.Hq; a.Hkv = s.Hkv; a.Sq = s.Sq; a.Skv = s.Skv; a.D = s.D;
+    a.G = G;
+    a.R = R;
+    a.T = T;
+    a.P = P;
+    a.c = scale * ef::kLog2e;
+    a.causal = causal ? 1 : 0;
+    return from_hip(ef::launch_decode_split(a, hs));
+  }
+  return launch_mfma(s, q, k, v, nullptr, ws_m, ws_l, ws_acc, T, P, scale, causal, hs);
+}
+
+}  // namespace
+
+extern "C" {
+
+ef_status ef_attention_splitkv_partials(const void* q, const void* k, const void* v, int B,
+                                        int Hq, int Hkv, int Sq, int Skv, int D, float scale,
+                                        int causal, int partition_size, void* workspace,
+                                        size_t workspace_bytes, void* stream) {
+  const Shape s{B, Hq, Hkv, Sq, Skv, D};
+  int T = 0, P = 0;
+  float *ws_m = nullptr, *ws_l = nullptr, *ws_acc = nullptr;
+  // The output pointer is not used here; pass q so the shared check sees a non-null pointer.
+  ef_status st = split_prepare(s, q, k, v, static_cast<const float*>(q), scale, partition_size,
+                               workspace, workspace_bytes, &T, &P, &ws_m, &ws_l, &ws_acc);
+  if (st != EF_OK || P == 0) return st;
+  return split_produce(s, q, k, v, scale, causal, T, P, ws_m, ws_l, ws_acc,
+                       static_cast<hipStream_t>(stream));
+}
+
+ef_status ef_attention_splitkv(const void* q, const void* k, const void* v, float* o, int B,
+                               int Hq, int Hkv, int Sq, int Skv, int D, float scale, int causal,
+                               int partition_size, void* workspace, size_t workspace_bytes,
+                               void* stream) {
+  const Shape s{B, Hq, Hkv, Sq, Skv, D};
+  int T = 0, P = 0;
+  float *ws_m = nullptr, *ws_l = nullptr, *ws_acc = nullptr;
+  ef_status st = split_prepare(s, q, k, v, o, scale, partition_size, workspace, workspace_bytes,
+                               &T, &P, &ws_m, &ws_l, &ws_acc);
+  if (st != EF_OK || s.rows() == 0) return st;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (Skv == 0) return from_hip(ef::launch_zero_fill(o, (size_t)s.rows() * D, hs));
+  st = split_produce(s, q, k, v, scale, causal, T, P, ws_m, ws_l, ws_acc, hs);
+  if (st != EF_OK) return st;
+  ef::CombineParams c{};
+  c.m = ws_m;
+  c.l = ws_l;
+  c.acc = ws_acc;
+  c.o = o;
+  c.rows = (int)s.rows();
+  c.P = P;
+  c.D = D;
+  return from_hip(ef::launch_combine(c, hs));
+}
+
+ef_status ef_attention_combine(const float* m, const float* l, const float* acc, float* o,
+                               int rows, int num_partitions, int D, void* stream) {
+  if (rows < 0 || num_partitions < 1) return EF_ERR_INVALID_SHAPE;
+  if (D != 64 && D != 128) return EF_ERR_UNSUPPORTED_HEAD_DIM;
+  if (rows == 0) return EF_OK;
+  if (m == nullptr || l == nullptr || acc == nullptr || o == nullptr) return EF_ERR_NULL_POINTER;
+  if (misaligned(m) || misaligned(l) || misaligned(acc) || misaligned(o)) return EF_ERR_MISALIGNED;
+  ef::CombineParams c{};
+  c.m = m;
+  c.l = l;
+  c.acc = acc;
+  c.o = o;
+  c.rows = rows;
+  c.P = num_partitions;
+  c.D = D;
+  return from_hip(ef::launch_combine(c, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

@@ -1,0 +1,214 @@
+// Split-KV decode producer for few query rows per kv head (G*Sq <= 8).
+//
+// One workgroup owns (partition p, kv head, batch): it streams the partition's
+// K and V rows from HBM exactly once with 128-bit loads and evaluates every
+// query row that reads this kv head (grouped-query replication by index,
+// section 3.1 "Replicate"). The rolling (max, sum, value) reducer of form M2
+// (section 3, figure "attention-rewrites"; section 4.2 repair fusion) runs in
+// registers, and the reduced state of the partition is stored for a later
+// combine (section 3.3 "Collection"; section 4.4 storage rule).
+//
+// Lane layout: a key row of D bf16 is read by D/8 adjacent lanes, 16 bytes
+// each, so one wave-wide load covers 64*16 contiguous bytes (4 rows at
+// D = 128). Every lane keeps its 8-element slice of each query row; q.k is a
+// packed-bf16 dot product followed by a DPP sum over the row's lanes, so all
+// lanes of a row group end up with the full score. Each row group carries its
+// own rolling state; the groups of a wave and the waves of the workgroup are
+// merged with the same reducer at the end.
+#include "ef_device.hpp"
+#include "ef_kernels.hpp"
+
+namespace ef {
+
+template <int D, int RMAX, int NW, int U>
+__global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
+  constexpr int LPR = D / 8;     // lanes per key row
+  constexpr int TPL = 64 / LPR;  // key rows per wave-wide load
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int tl = lane / LPR;  // row slot inside a wave-wide load
+  const int dc = lane % LPR;  // which 8-element slice of D this lane holds
+  const int p = blockIdx.x, hkv = blockIdx.y, b = blockIdx.z;
+  const int t0 = p * a.T;
+  const int t1 = min(t0 + a.T, a.Skv);
+  const size_t kvhead = ((size_t)b * a.Hkv + hkv) * (size_t)a.Skv;
+  const uint4* kp = reinterpret_cast<const uint4*>(a.k + kvhead * D) + dc;
+  const uint4* vp = reinterpret_cast<const uint4*>(a.v + kvhead * D) + dc;
+  // Query rows of this kv head are contiguous: row r = g*Sq + sq.
+  const size_t row0 = ((size_t)b * a.Hq + (size_t)hkv * a.G) * (size_t)a.Sq;
+
+  uint32_t qv[RMAX][4];
+  int lim[RMAX];
+#pragma unroll
+  for (int r = 0; r < RMAX; ++r) {
+    if (r < a.R) {
+      uint4 x = reinterpret_cast<const uint4*>(a.q + (row0 + r) * D)[dc];
+      qv[r][0] = x.x; qv[r][1] = x.y; qv[r][2] = x.z; qv[r][3] = x.w;
+      lim[r] = a.causal ? (r % a.Sq) + a.Skv - a.Sq : 0x7fffffff;
+    } else {
+      qv[r][0] = qv[r][1] = qv[r][2] = qv[r][3] = 0u;
+      lim[r] = -1;  // padding row: every key masked
+    }
+  }
+
+  float m[RMAX], l[RMAX], acc[RMAX][8];
+#pragma unroll
+  for (int r = 0; r < RMAX; ++r) {
+    m[r] = kNegInf;
+    l[r] = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[r][e] = 0.f;
+  }
+
+  const float c = a.c;  // scale * log2(e): scores are kept in base-2 units
+  constexpr int STEP = NW * TPL;  // key rows per workgroup-wide load
+  for (int tb = t0; tb < t1; tb += U * STEP) {
+    uint4 kr[U], vr[U];
+    int tok[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      tok[u] = tb + (u * NW + wave) * TPL + tl;
+      if (tok[u] < t1) {
+        kr[u] = load_nt16(kp + (size_t)tok[u] * LPR);
+      } else {
+        kr[u] = make_uint4(0u, 0u, 0u, 0u);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      if (tok[u] < t1) {
+        vr[u] = load_nt16(vp + (size_t)tok[u] * LPR);
+      } else {
+        vr[u] = make_uint4(0u, 0u, 0u, 0u);
+      }
+    }
+    // Scores in base-2 units, masked to -inf where the key is not visible.
+    float s[U][RMAX];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+#pragma unroll
+      for (int r = 0; r < RMAX; ++r) {
+        float d = dot2_bf16(qv[r][0], kr[u].x, 0.f);
+        d = dot2_bf16(qv[r][1], kr[u].y, d);
+        d = dot2_bf16(qv[r][2], kr[u].z, d);
+        d = dot2_bf16(qv[r][3], kr[u].w, d);
+        d = group_sum<LPR>(d) * c;
+        s[u][r] = (tok[u] < t1 && tok[u] <= lim[r]) ? d : kNegInf;
+      }
+    }
+    float vf[U][8];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      vf[u][0] = bf16lo_to_f32(vr[u].x); vf[u][1] = bf16hi_to_f32(vr[u].x);
+      vf[u][2] = bf16lo_to_f32(vr[u].y); vf[u][3] = bf16hi_to_f32(vr[u].y);
+      vf[u][4] = bf16lo_to_f32(vr[u].z); vf[u][5] = bf16hi_to_f32(vr[u].z);
+      vf[u][6] = bf16lo_to_f32(vr[u].w); vf[u][7] = bf16hi_to_f32(vr[u].w);
+    }
+    // Rolling update: next_max, rescale of the carried state, new weights.
+#pragma unroll
+    for (int r = 0; r < RMAX; ++r) {
+      float bm = s[0][r];
+#pragma unroll
+      for (int u = 1; u < U; ++u) bm = fmaxf(bm, s[u][r]);
+      const float mn = fmaxf(m[r], bm);
+      const float ms = (mn == kNegInf) ? 0.f : mn;
+      const float rs = exp2_fast(m[r] - ms);
+      float psum = 0.f;
+      float pw[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        pw[u] = exp2_fast(s[u][r] - ms);
+        psum += pw[u];
+      }
+      l[r] = l[r] * rs + psum;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float x = acc[r][e] * rs;
+#pragma unroll
+        for (int u = 0; u < U; ++u) x = fmaf(pw[u], vf[u][e], x);
+        acc[r][e] = x;
+      }
+      m[r] = mn;
+    }
+  }
+
+  // Merge the row groups of the wave (lanes l and l ^ LPR*k hold the same D slice).
+#pragma unroll
+  for (int off = LPR; off < 64; off <<= 1) {
+#pragma unroll
+    for (int r = 0; r < RMAX; ++r) {
+      const float mo = shfl_xor(m[r], off);
+      const float lo = shfl_xor(l[r], off);
+      const float mn = fmaxf(m[r], mo);
+      const float ms = (mn == kNegInf) ? 0.f : mn;
+      const float wa = exp2_fast(m[r] - ms), wb = exp2_fast(mo - ms);
+      l[r] = l[r] * wa + lo * wb;
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const float ao = shfl_xor(acc[r][e], off);
+        acc[r][e] = acc[r][e] * wa + ao * wb;
+      }
+      m[r] = mn;
+    }
+  }
+
+  // Merge the waves through LDS and store the partition's state.
+  __shared__ float sm[NW][RMAX], sl[NW][RMAX];
+  __shared__ float sacc[NW][RMAX][D];
+  if (tl == 0) {
+#pragma unroll
+    for (int r = 0; r < RMAX; ++r) {
+      if (dc == 0) {
+        sm[wave][r] = m[r];
+        sl[wave][r] = l[r];
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) sacc[wave][r][dc * 8 + e] = acc[r][e];
+    }
+  }
+  __syncthreads();
+  const int P = a.P;
+  for (int idx = threadIdx.x; idx < a.R * D; idx += NW * 64) {
+    const int r = idx / D, d = idx % D;
+    float M = kNegInf;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) M = fmaxf(M, sm[w][r]);
+    const float ms = (M == kNegInf) ? 0.f : M;
+    float L = 0.f, A = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      const float wt = exp2_fast(sm[w][r] - ms);
+      L = fmaf(wt, sl[w][r], L);
+      A = fmaf(wt, sacc[w][r][d], A);
+    }
+    const size_t slot = (row0 + r) * (size_t)P + p;
+    a.ws_acc[slot * D + d] = A;
+    if (d == 0) {
+      a.ws_m[slot] = (M == kNegInf) ? kNegInf : M * kLn2;  // natural-log units
+      a.ws_l[slot] = L;
+    }
+  }
+}
+
+template <int D, int RMAX>
+static hipError_t launch_decode_r(const DecodeParams& a, hipStream_t stream) {
+  constexpr int NW = 4;
+  constexpr int U = RMAX <= 2 ? 4 : (RMAX <= 4 ? 4 : 2);
+  dim3 grid(a.P, a.Hkv, a.B);
+  hipLaunchKernelGGL((decode_split_kernel<D, RMAX, NW, U>), grid, dim3(NW * 64), 0, stream, a);
+  return hipGetLastError();
+}
+
+template <int D>
+static hipError_t launch_decode_d(const DecodeParams& a, hipStream_t stream) {
+  if (a.R <= 1) return launch_decode_r<D, 1>(a, stream);
+  if (a.R <= 2) return launch_decode_r<D, 2>(a, stream);
+  if (a.R <= 4) return launch_decode_r<D, 4>(a, stream);
+  return launch_decode_r<D, 8>(a, stream);
+}
+
+hipError_t launch_decode_split(const DecodeParams& a, hipStream_t stream) {
+  return a.D == 128 ? launch_decode_d<128>(a, stream) : launch_decode_d<64>(a, stream);
+}
+
+}  // namespace ef

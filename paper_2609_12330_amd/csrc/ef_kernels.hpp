@@ -1,0 +1,61 @@
+// Kernel parameter blocks and launchers of the gfx950 attention library.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ef {
+
+// Split-KV decode producer (VALU path, G*Sq <= 8 query rows per kv head).
+struct DecodeParams {
+  const uint16_t* q;  // [B][Hq][Sq][D] bf16
+  const uint16_t* k;  // [B][Hkv][Skv][D] bf16
+  const uint16_t* v;
+  float* ws_m;    // [rows][P]
+  float* ws_l;    // [rows][P]
+  float* ws_acc;  // [rows][P][D]
+  int B, Hq, Hkv, Sq, Skv, D;
+  int G;  // Hq / Hkv
+  int R;  // G * Sq query rows per kv head
+  int T;  // keys per partition
+  int P;  // partitions
+  float c;  // scale * log2(e)
+  int causal;
+};
+
+// MFMA attention (single pass, or split producer when ws_m != nullptr).
+struct MfmaParams {
+  const uint16_t* q;
+  const uint16_t* k;
+  const uint16_t* v;
+  float* o;       // [B][Hq][Sq][D] fp32, single-pass mode
+  float* ws_m;    // split mode: partial states as in DecodeParams
+  float* ws_l;
+  float* ws_acc;
+  int B, Hq, Hkv, Sq, Skv, D;
+  int G, R;
+  int T, P;      // keys per partition and partitions (T >= Skv, P = 1 in single-pass mode)
+  int mtiles;    // query-row tiles per kv head
+  float c_abs;   // |scale| * log2(e)
+  int causal;
+};
+
+// Combine of stored partial states.
+struct CombineParams {
+  const float* m;
+  const float* l;
+  const float* acc;
+  float* o;  // [rows][D]
+  int rows, P, D;
+};
+
+// Fill of an fp32 buffer with zeros (output rows that see no key).
+hipError_t launch_zero_fill(float* p, size_t n, hipStream_t stream);
+hipError_t launch_decode_split(const DecodeParams& a, hipStream_t stream);
+hipError_t launch_mfma_attention(const MfmaParams& a, bool negative_scale, hipStream_t stream);
+hipError_t launch_combine(const CombineParams& a, hipStream_t stream);
+
+// Rows per workgroup of the MFMA kernel for a problem with R rows per kv head.
+int mfma_rows_per_block(int R);
+
+}  // namespace ef

@@ -1,0 +1,272 @@
+"""ctypes binding of ``libef_attention.so`` (C ABI in include/ef_attention.h).
+
+Argument marshalling only: every step of the attention runs in the HIP
+kernels of the library. torch provides device memory and the current stream.
+The functions raise ``RuntimeError`` when the library is missing (build it
+with ``python -m paper_2609_12330_amd.build``) and ``EfError`` when the
+library rejects its arguments.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "lib", "libef_attention.so")
+
+EF_OK = 0
+STATUS_NAMES = {
+    0: "EF_OK",
+    1: "EF_ERR_NULL_POINTER",
+    2: "EF_ERR_INVALID_SHAPE",
+    3: "EF_ERR_GQA_RATIO",
+    4: "EF_ERR_UNSUPPORTED_HEAD_DIM",
+    5: "EF_ERR_MISALIGNED",
+    6: "EF_ERR_INVALID_PARTITION",
+    7: "EF_ERR_WORKSPACE_TOO_SMALL",
+    8: "EF_ERR_INVALID_SCALE",
+    9: "EF_ERR_HIP",
+}
+
+# Exported symbols and their C signatures (restype, argtypes).
+_vp, _fp, _i, _f, _sz = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+SIGNATURES = {
+    "ef_abi_version": (_i, []),
+    "ef_status_string": (ctypes.c_char_p, [_i]),
+    "ef_attention_fwd": (_i, [_vp, _vp, _vp, _fp, _i, _i, _i, _i, _i, _i, _f, _i, _vp]),
+    "ef_attention_splitkv_partition_size": (_i, [_i, _i, _i, _i, _i, _i, _i]),
+    "ef_attention_splitkv_workspace_size": (_sz, [_i, _i, _i, _i, _i, _i, _i]),
+    "ef_attention_splitkv": (_i, [_vp, _vp, _vp, _fp, _i, _i, _i, _i, _i, _i, _f, _i, _i,
+                                  _vp, _sz, _vp]),
+    "ef_attention_splitkv_partials": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _f, _i, _i,
+                                           _vp, _sz, _vp]),
+    "ef_attention_combine": (_i, [_fp, _fp, _fp, _fp, _i, _i, _i, _vp]),
+}
+
+
+class EfError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        msg = _lib().ef_status_string(status).decode()
+        super().__init__(f"{where}: {STATUS_NAMES.get(status, status)} ({msg})")
+
+
+_LIB = None
+
+
+def _lib():
+    global _LIB
+    if _LIB is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(
+                f"HIP library not built: {LIB_PATH} is missing "
+                "(run python -m paper_2609_12330_amd.build)")
+        lib = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _LIB = lib
+    return _LIB
+
+
+def library():
+    """The loaded ctypes library (loads it on first use)."""
+    return _lib()
+
+
+def _check(status: int, where: str):
+    if status != EF_OK:
+        raise EfError(status, where)
+
+
+# ---------------------------------------------------------------------------
+# Raw pointer-level calls (same names and arguments as the C ABI).
+# ---------------------------------------------------------------------------
+
+
+def ef_attention_fwd(q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale, causal, stream) -> int:
+    return _lib().ef_attention_fwd(q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale, int(causal), stream)
+
+
+def ef_attention_splitkv(q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale, causal, partition_size,
+                         workspace, workspace_bytes, stream) -> int:
+    return _lib().ef_attention_splitkv(q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale, int(causal),
+                                       partition_size, workspace, workspace_bytes, stream)
+
+
+def ef_attention_splitkv_partials(q, k, v, B, Hq, Hkv, Sq, Skv, D, scale, causal, partition_size,
+                                  workspace, workspace_bytes, stream) -> int:
+    return _lib().ef_attention_splitkv_partials(q, k, v, B, Hq, Hkv, Sq, Skv, D, scale,
+                                                int(causal), partition_size, workspace,
+                                                workspace_bytes, stream)
+
+
+def ef_attention_combine(m, l, acc, o, rows, num_partitions, D, stream) -> int:
+    return _lib().ef_attention_combine(m, l, acc, o, rows, num_partitions, D, stream)
+
+
+def ef_attention_splitkv_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size) -> int:
+    return _lib().ef_attention_splitkv_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size)
+
+
+def ef_attention_splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, partition_size) -> int:
+    return _lib().ef_attention_splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, partition_size)
+
+
+# ---------------------------------------------------------------------------
+# torch-tensor conveniences
+# ---------------------------------------------------------------------------
+
+
+def _torch():
+    import torch
+    return torch
+
+
+def _stream_handle(stream) -> Optional[int]:
+    torch = _torch()
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+def _check_qkv(q, k, v):
+    torch = _torch()
+    for name, t in (("q", q), ("k", k), ("v", v)):
+        if t.dtype != torch.bfloat16:
+            raise TypeError(f"{name} must be bfloat16, got {t.dtype}")
+        if not t.is_cuda:
+            raise TypeError(f"{name} must be a GPU tensor")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous [B, H, S, D]")
+        if t.dim() != 4:
+            raise ValueError(f"{name} must be 4-D [B, H, S, D]")
+    B, Hq, Sq, D = q.shape
+    if k.shape != v.shape or k.shape[0] != B or k.shape[3] != D:
+        raise ValueError("k and v must be [B, Hkv, Skv, D] matching q")
+    return B, Hq, k.shape[1], Sq, k.shape[2], D
+
+
+def _out(q, out):
+    torch = _torch()
+    if out is None:
+        return torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    if out.dtype != torch.float32 or out.shape != q.shape or not out.is_contiguous():
+        raise ValueError("out must be a contiguous fp32 tensor shaped like q")
+    _same_device(out, q, "out")
+    return out
+
+
+def _same_device(t, ref, name):
+    if not t.is_cuda or t.device != ref.device:
+        raise TypeError(f"{name} must be a GPU tensor on {ref.device}, got {t.device}")
+
+
+def _check_workspace(ws, q):
+    _same_device(ws, q, "workspace")
+    if not ws.is_contiguous():
+        raise ValueError("workspace must be contiguous")
+
+
+def attention_fwd(q, k, v, scale: Optional[float] = None, causal: bool = False, out=None,
+                  stream=None):
+    """o = softmax(scale * q k^T [masked]) v in fp32 through ef_attention_fwd."""
+    B, Hq, Hkv, Sq, Skv, D = _check_qkv(q, k, v)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    o = _out(q, out)
+    st = ef_attention_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B, Hq, Hkv, Sq,
+                          Skv, D, float(scale), causal, _stream_handle(stream))
+    _check(st, "ef_attention_fwd")
+    return o
+
+
+def splitkv_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size=0) -> int:
+    return int(ef_attention_splitkv_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size))
+
+
+def splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, partition_size=0) -> int:
+    return int(ef_attention_splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, partition_size))
+
+
+def make_workspace(q, k, partition_size=0):
+    """A uint8 tensor on q's GPU large enough for attention_splitkv on these shapes."""
+    torch = _torch()
+    if not q.is_cuda:
+        raise TypeError("make_workspace needs GPU tensors (the workspace lives on q's device)")
+    B, Hq, Sq, D = q.shape
+    Hkv, Skv = k.shape[1], k.shape[2]
+    n = splitkv_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size)
+    return torch.empty(max(n, 256), dtype=torch.uint8, device=q.device)
+
+
+def workspace_views(ws, B, Hq, Sq, Skv, D, T):
+    """(m [rows,P], l [rows,P], acc [rows,P,D]) fp32 views of a split-KV workspace."""
+    rows = B * Hq * Sq
+    P = -(-Skv // T)
+    a = (rows * P * 4 + 255) // 256 * 256
+    f = ws.view(_torch().float32) if ws.dtype != _torch().float32 else ws
+    m = f[: rows * P].view(rows, P)
+    l = f[a // 4: a // 4 + rows * P].view(rows, P)
+    acc = f[2 * a // 4: 2 * a // 4 + rows * P * D].view(rows, P, D)
+    return m, l, acc
+
+
+def attention_splitkv(q, k, v, scale: Optional[float] = None, causal: bool = False,
+                      partition_size: int = 0, workspace=None, out=None, stream=None):
+    """Split-KV attention through ef_attention_splitkv; returns o (fp32)."""
+    B, Hq, Hkv, Sq, Skv, D = _check_qkv(q, k, v)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    o = _out(q, out)
+    if workspace is None:
+        workspace = make_workspace(q, k, partition_size)
+    _check_workspace(workspace, q)
+    st = ef_attention_splitkv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B, Hq, Hkv,
+                              Sq, Skv, D, float(scale), causal, partition_size,
+                              workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                              _stream_handle(stream))
+    _check(st, "ef_attention_splitkv")
+    return o
+
+
+def attention_splitkv_partials(q, k, v, scale: Optional[float] = None, causal: bool = False,
+                               partition_size: int = 0, workspace=None, stream=None):
+    """Producer step only: fills and returns the workspace with the partial states."""
+    B, Hq, Hkv, Sq, Skv, D = _check_qkv(q, k, v)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    if workspace is None:
+        workspace = make_workspace(q, k, partition_size)
+    _check_workspace(workspace, q)
+    st = ef_attention_splitkv_partials(q.data_ptr(), k.data_ptr(), v.data_ptr(), B, Hq, Hkv, Sq,
+                                       Skv, D, float(scale), causal, partition_size,
+                                       workspace.data_ptr(),
+                                       workspace.numel() * workspace.element_size(),
+                                       _stream_handle(stream))
+    _check(st, "ef_attention_splitkv_partials")
+    return workspace
+
+
+def combine(m, l, acc, out=None, stream=None):
+    """Combine fp32 partial states m [rows,P], l [rows,P], acc [rows,P,D] into o [rows,D]."""
+    torch = _torch()
+    rows, P, D = acc.shape
+    for name, t in (("m", m), ("l", l), ("acc", acc)):
+        if t.dtype != torch.float32 or not t.is_cuda or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous fp32 GPU tensor")
+    if m.shape != (rows, P) or l.shape != (rows, P):
+        raise ValueError("m and l must be [rows, P]")
+    o = torch.empty(rows, D, dtype=torch.float32, device=acc.device) if out is None else out
+    for name, t in (("m", m), ("l", l), ("out", o)):
+        _same_device(t, acc, name)
+    if o.dtype != torch.float32 or o.shape != (rows, D) or not o.is_contiguous():
+        raise ValueError("out must be a contiguous fp32 [rows, D] tensor")
+    st = ef_attention_combine(m.data_ptr(), l.data_ptr(), acc.data_ptr(), o.data_ptr(), rows, P, D,
+                              _stream_handle(stream))
+    _check(st, "ef_attention_combine")
+    return o

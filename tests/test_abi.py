@@ -1,0 +1,169 @@
+"""The C-ABI library on the CPU: it loads, exports every symbol the header
+declares, and rejects bad arguments on the host before any HIP call.
+
+Only error paths and pure-host queries run here (no GPU in this container):
+each rejected call returns before the library touches the HIP runtime.
+"""
+
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+from paper_2609_12330_amd import ef_attention as ef
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ef_attention.h")
+
+needs_lib = pytest.mark.skipif(not os.path.exists(ef.LIB_PATH),
+                               reason="libef_attention.so not built")
+
+# Fake device addresses: non-null, 16-byte aligned; never dereferenced on these paths.
+A = 0x10000
+MIS = 0x10008
+
+
+def header_functions():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(ef_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_header_declares_the_entry_points():
+    names = header_functions()
+    for n in ("ef_attention_fwd", "ef_attention_splitkv", "ef_attention_combine",
+              "ef_attention_splitkv_workspace_size", "ef_attention_splitkv_partition_size",
+              "ef_status_string", "ef_abi_version"):
+        assert n in names
+    assert set(names) == set(ef.SIGNATURES), "binding signatures must cover the header exactly"
+
+
+@needs_lib
+def test_library_exports_every_header_symbol():
+    lib = ctypes.CDLL(ef.LIB_PATH)
+    for name in header_functions():
+        assert hasattr(lib, name), name
+    assert ef.library().ef_abi_version() == 1
+
+
+@needs_lib
+def test_status_strings():
+    lib = ef.library()
+    for s in range(0, 10):
+        assert lib.ef_status_string(s)
+    assert lib.ef_status_string(0) == b"ok"
+    assert lib.ef_status_string(1234) == b"unknown status"
+
+
+def fwd(**kw):
+    a = dict(q=A, k=A, v=A, o=A, B=1, Hq=4, Hkv=2, Sq=8, Skv=16, D=128, scale=0.1, causal=0,
+             stream=None)
+    a.update(kw)
+    return ef.ef_attention_fwd(a["q"], a["k"], a["v"], a["o"], a["B"], a["Hq"], a["Hkv"],
+                               a["Sq"], a["Skv"], a["D"], a["scale"], a["causal"], a["stream"])
+
+
+def split(**kw):
+    a = dict(q=A, k=A, v=A, o=A, B=1, Hq=4, Hkv=2, Sq=1, Skv=1000, D=128, scale=0.1, causal=0,
+             T=256, ws=A, wsb=1 << 30, stream=None)
+    a.update(kw)
+    return ef.ef_attention_splitkv(a["q"], a["k"], a["v"], a["o"], a["B"], a["Hq"], a["Hkv"],
+                                   a["Sq"], a["Skv"], a["D"], a["scale"], a["causal"], a["T"],
+                                   a["ws"], a["wsb"], a["stream"])
+
+
+@needs_lib
+@pytest.mark.parametrize("call", [fwd, split], ids=["fwd", "splitkv"])
+def test_validation_errors(call):
+    assert call(D=96) == 4
+    assert call(D=0) == 4
+    assert call(Hq=6, Hkv=4) == 3
+    assert call(Hkv=0) == 2
+    assert call(Hq=0) == 2
+    assert call(B=-1) == 2
+    assert call(Sq=-3) == 2
+    assert call(Skv=-1) == 2
+    assert call(q=None) == 1
+    assert call(o=None) == 1
+    assert call(k=None) == 1
+    assert call(v=None) == 1
+    assert call(q=MIS) == 5
+    assert call(k=MIS) == 5
+    assert call(o=MIS) == 5
+    assert call(scale=math.inf) == 8
+    assert call(scale=math.nan) == 8
+    assert call(Skv=1 << 24) == 2  # Skv * D reaches 2^31 elements per head
+    assert call(B=70000, Hkv=1, Hq=1) == 2  # B * Hkv beyond the grid
+    # empty problems are accepted and enqueue nothing
+    assert call(B=0) == 0
+    assert call(Sq=0) == 0
+    assert call(B=0, q=None, o=None) == 0
+
+
+@needs_lib
+def test_splitkv_specific_validation():
+    assert split(T=100) == 6
+    assert split(T=-64) == 6
+    assert split(ws=None) == 7
+    need = ef.ef_attention_splitkv_workspace_size(1, 4, 2, 1, 1000, 128, 256)
+    assert split(wsb=need - 1) == 7
+    assert split(ws=MIS, wsb=need) == 5
+
+
+@needs_lib
+def test_combine_validation():
+    c = ef.ef_attention_combine
+    assert c(A, A, A, A, -1, 4, 128, None) == 2
+    assert c(A, A, A, A, 4, 0, 128, None) == 2
+    assert c(A, A, A, A, 4, 4, 32, None) == 4
+    assert c(None, A, A, A, 4, 4, 128, None) == 1
+    assert c(A, A, A, None, 4, 4, 128, None) == 1
+    assert c(A, MIS, A, A, 4, 4, 128, None) == 5
+    assert c(None, None, None, None, 0, 4, 128, None) == 0
+
+
+@needs_lib
+def test_workspace_and_partition_arithmetic():
+    ws = ef.ef_attention_splitkv_workspace_size
+    ps = ef.ef_attention_splitkv_partition_size
+    # GQA decode, 256-key partitions: rows = 8*32, P = 16
+    rows, P, D = 256, 16, 128
+    a = (rows * P * 4 + 255) // 256 * 256
+    assert ws(8, 32, 8, 1, 4096, 128, 256) == 2 * a + rows * P * D * 4
+    # 131072 keys, 512 partitions of 256
+    rows, P = 32, 512
+    a = (rows * P * 4 + 255) // 256 * 256
+    assert ws(1, 32, 8, 1, 131072, 128, 256) == 2 * a + rows * P * D * 4
+    # ragged: 1000 keys in partitions of 256 -> P = 4
+    rows, P = 4, 4
+    a = (rows * P * 4 + 255) // 256 * 256
+    assert ws(1, 4, 2, 1, 1000, 128, 256) == 2 * a + rows * P * 128 * 4
+    assert ps(1, 4, 2, 1, 1000, 128, 256) == 256
+    # the library's choice is a multiple of 64 covering Skv with B*Hkv*P near 1024 blocks
+    t = ps(8, 32, 8, 1, 4096, 128, 0)
+    assert t > 0 and t % 64 == 0
+    t = ps(16, 64, 8, 8, 8192, 128, 0)
+    assert t % 64 == 0 and 16 * 8 * (-(-8192 // t)) >= 512
+    assert ps(1, 4, 2, 1, 1000, 96, 0) == 0
+    assert ps(1, 4, 2, 1, 1000, 128, 100) == 0
+    assert ws(1, 4, 2, 1, 1000, 128, 100) == 0
+    assert ws(0, 4, 2, 1, 1000, 128, 256) == 0
+    assert ws(1, 4, 2, 1, 0, 128, 256) == 0
+
+
+def test_binding_fails_loudly_without_library(monkeypatch):
+    monkeypatch.setattr(ef, "_LIB", None)
+    monkeypatch.setattr(ef, "LIB_PATH", "/nonexistent/libef_attention.so")
+    with pytest.raises(RuntimeError, match="not built"):
+        ef.library()
+
+
+def test_product_path_never_imports_the_oracle():
+    pkg = os.path.join(ROOT, "paper_2609_12330_amd")
+    for dirpath, _, files in os.walk(pkg):
+        for f in files:
+            if f.endswith((".py", ".hip", ".hpp", ".cpp", ".h")):
+                src = open(os.path.join(dirpath, f)).read()
+                assert "import oracle" not in src and "from oracle" not in src, f

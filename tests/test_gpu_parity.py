@@ -1,0 +1,355 @@
+"""GPU parity of the HIP path (through the C ABI) against the fp64 oracle.
+
+Bar: max |o - ref| <= 1e-2 and mean |o - ref| <= 1e-3 over every output for
+bf16 inputs; the fp32 combine is within 1e-5 of the fp64 combine of the same
+fp32 partial states, relative to the magnitude (sum_p w_p |acc_p|) / L that
+bounds its rounding. The oracle runs on the exact bf16 input values widened to
+fp64. Every case prints its name before it touches the GPU.
+"""
+
+import math
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_12330_amd import ef_attention as ef
+from paper_2609_12330_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS = 1e-2
+MEAN_ABS = 1e-3
+COMBINE_REL = 1e-5
+
+
+def announce(msg):
+    print(f"[gpu case] {msg}", file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    if not os.path.exists(ef.LIB_PATH):
+        raise RuntimeError("libef_attention.so is not built; the HIP path must be present")
+    ef.library()
+    yield
+
+
+def inputs(B, Hq, Hkv, Sq, Skv, D, seed, q_mult=1.0):
+    q, k, v = wl.make_shape_inputs(B, Hq, Hkv, Sq, Skv, D, seed, q_mult=q_mult)
+    return q, k, v
+
+
+def f64(t):
+    return wl.to_f64(t)
+
+
+def assert_close(o, ref, what):
+    o = o.detach().cpu().double().numpy() if isinstance(o, torch.Tensor) else o
+    assert np.isfinite(o).all(), f"{what}: non-finite output"
+    d = np.abs(o - ref)
+    mx, mean = float(d.max()) if d.size else 0.0, float(d.mean()) if d.size else 0.0
+    rel_l2 = float(np.linalg.norm(o - ref) / max(np.linalg.norm(ref), 1e-30)) if d.size else 0.0
+    assert mx <= MAX_ABS and mean <= MEAN_ABS, (
+        f"{what}: max {mx:.3e} mean {mean:.3e} rel-L2 {rel_l2:.3e}")
+    return mx, mean, rel_l2
+
+
+def run_fwd(q, k, v, scale, causal):
+    return ef.attention_fwd(q.cuda(), k.cuda(), v.cuda(), scale=scale, causal=causal)
+
+
+def run_split(q, k, v, scale, causal, T):
+    return ef.attention_splitkv(q.cuda(), k.cuda(), v.cuda(), scale=scale, causal=causal,
+                                partition_size=T)
+
+
+# ---------------------------------------------------------------------------
+# Small and ragged shapes: several tiles, ragged tails, GQA ratios 1..8, D 64/128.
+# ---------------------------------------------------------------------------
+
+FWD_SHAPES = [
+    # B, Hq, Hkv, Sq, Skv, D
+    (1, 4, 4, 64, 64, 64),
+    (1, 4, 2, 200, 200, 128),
+    (2, 8, 2, 70, 333, 128),
+    (1, 2, 2, 129, 65, 64),     # Sq > Skv: causal rows that see nothing
+    (1, 8, 1, 5, 300, 128),     # G = 8, few query rows
+    (1, 1, 1, 1, 1, 128),
+    (1, 4, 4, 64, 1000, 64),
+    (1, 16, 2, 40, 130, 128),   # G = 8, 320 packed rows, ragged row tile
+]
+
+
+@pytest.mark.parametrize("shape", FWD_SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("causal", [False, True])
+def test_fwd_small(shape, causal):
+    B, Hq, Hkv, Sq, Skv, D = shape
+    announce(f"fwd {shape} causal={causal}")
+    q, k, v = inputs(*shape, seed=100 + sum(shape))
+    scale = 1.0 / math.sqrt(D)
+    o = run_fwd(q, k, v, scale, causal)
+    torch.cuda.synchronize()
+    ref = oracle.attention_ref(f64(q), f64(k), f64(v), scale, causal)
+    assert_close(o, ref, f"fwd {shape} causal={causal}")
+
+
+SPLIT_SHAPES = [
+    # B, Hq, Hkv, Sq, Skv, D, T
+    (2, 8, 2, 1, 1000, 128, 256),   # G*Sq = 4: VALU producer, ragged last partition
+    (1, 4, 4, 2, 777, 128, 64),     # G*Sq = 2
+    (1, 16, 2, 1, 513, 64, 128),    # G*Sq = 8, D = 64
+    (3, 2, 2, 1, 70, 128, 64),      # G*Sq = 1
+    (2, 16, 2, 3, 900, 128, 256),   # G*Sq = 24: MFMA producer
+    (1, 8, 1, 8, 2000, 128, 0),     # G*Sq = 64: MFMA producer, library-chosen partitions
+    (1, 4, 2, 1, 64, 128, 64),      # one partition
+    (1, 32, 4, 5, 333, 64, 128),    # G*Sq = 40, D = 64
+]
+
+
+@pytest.mark.parametrize("shape", SPLIT_SHAPES, ids=lambda s: "x".join(map(str, s)))
+@pytest.mark.parametrize("causal", [False, True])
+def test_splitkv_small(shape, causal):
+    B, Hq, Hkv, Sq, Skv, D, T = shape
+    announce(f"splitkv {shape} causal={causal}")
+    q, k, v = inputs(B, Hq, Hkv, Sq, Skv, D, seed=200 + sum(shape))
+    scale = 1.0 / math.sqrt(D)
+    o = run_split(q, k, v, scale, causal, T)
+    torch.cuda.synchronize()
+    ref = oracle.attention_ref(f64(q), f64(k), f64(v), scale, causal)
+    assert_close(o, ref, f"splitkv {shape} causal={causal}")
+
+
+@pytest.mark.parametrize("path", ["fwd", "splitkv"])
+def test_negative_scale(path):
+    announce(f"negative scale {path}")
+    q, k, v = inputs(1, 8, 2, 3, 300, 128, seed=7)
+    scale = -0.09
+    o = run_fwd(q, k, v, scale, True) if path == "fwd" else run_split(q, k, v, scale, True, 64)
+    torch.cuda.synchronize()
+    ref = oracle.attention_ref(f64(q), f64(k), f64(v), scale, True)
+    assert_close(o, ref, f"negative scale {path}")
+
+
+def test_sharp_softmax_large_logits():
+    """q scaled by 16: logits span hundreds, the reference point moves often."""
+    announce("sharp softmax")
+    q, k, v = inputs(1, 4, 2, 50, 700, 128, seed=8, q_mult=16.0)
+    scale = 1.0 / math.sqrt(128)
+    ref = oracle.attention_ref(f64(q), f64(k), f64(v), scale, True)
+    assert_close(run_fwd(q, k, v, scale, True), ref, "sharp fwd")
+    assert_close(run_split(q[:, :, -1:], k, v, scale, True, 128),
+                 oracle.attention_ref(f64(q[:, :, -1:]), f64(k), f64(v), scale, True), "sharp split")
+
+
+# ---------------------------------------------------------------------------
+# The five workloads at full size.
+# ---------------------------------------------------------------------------
+
+
+def test_config_tiny_mha():
+    cfg = wl.CONFIGS[0]
+    announce(cfg.name)
+    q, k, v = wl.make_inputs(cfg, wl.DEFAULT_SEED[cfg.name])
+    ref = oracle.attention_ref(f64(q), f64(k), f64(v), cfg.scale, cfg.causal)
+    assert_close(run_fwd(q, k, v, cfg.scale, cfg.causal), ref, "tiny fwd")
+    assert_close(run_split(q, k, v, cfg.scale, cfg.causal, 0), ref, "tiny split")
+
+
+@pytest.mark.parametrize("idx", [1, 3, 4])
+@pytest.mark.parametrize("seed_offset", [0, 10])
+def test_config_decode_full(idx, seed_offset):
+    """Split-KV decode workloads, every output checked against the full oracle."""
+    cfg = wl.CONFIGS[idx]
+    seed = wl.DEFAULT_SEED[cfg.name] + seed_offset
+    announce(f"{cfg.name} seed {seed}")
+    q, k, v = wl.make_inputs(cfg, seed)
+    o = run_split(q, k, v, cfg.scale, cfg.causal, cfg.partition_size)
+    torch.cuda.synchronize()
+    ref = oracle.attention_ref(f64(q), f64(k), f64(v), cfg.scale, cfg.causal)
+    assert_close(o, ref, cfg.name)
+
+
+def test_config_prefill_sampled_heads():
+    """Causal GQA prefill at full size; the oracle evaluates 6 sampled query heads whole."""
+    cfg = wl.CONFIGS[2]
+    announce(cfg.name)
+    q, k, v = wl.make_inputs(cfg, wl.DEFAULT_SEED[cfg.name])
+    o = run_fwd(q, k, v, cfg.scale, cfg.causal).cpu()
+    torch.cuda.synchronize()
+    G = cfg.G
+    for b, hq in [(0, 0), (0, 5), (1, 17), (2, 31), (3, 8), (3, 26)]:
+        hk = hq // G
+        ref = oracle.attention_ref(f64(q[b:b + 1, hq:hq + 1]), f64(k[b:b + 1, hk:hk + 1]),
+                                   f64(v[b:b + 1, hk:hk + 1]), cfg.scale, True)
+        assert_close(o[b:b + 1, hq:hq + 1], ref, f"prefill b{b} hq{hq}")
+
+
+def test_config_prefill_split_matches_fwd():
+    """The same prefill through the split producer (MFMA, stored states) and the combine."""
+    cfg = wl.CONFIGS[2]
+    announce(cfg.name + " split")
+    q, k, v = wl.make_inputs(cfg, 33)
+    q, k, v = q[:1, :8], k[:1, :2], v[:1, :2]  # one batch, two kv heads
+    ref = oracle.attention_ref(f64(q), f64(k), f64(v), cfg.scale, True)
+    assert_close(run_split(q.contiguous(), k.contiguous(), v.contiguous(), cfg.scale, True, 512),
+                 ref, "prefill split")
+
+
+# ---------------------------------------------------------------------------
+# Combine of stored states, and the states themselves.
+# ---------------------------------------------------------------------------
+
+
+@pytest.mark.parametrize("P", [1, 2, 16, 512, 513])
+@pytest.mark.parametrize("D", [64, 128])
+def test_combine_fp32(P, D):
+    announce(f"combine P={P} D={D}")
+    rows = 64
+    m, l, acc = wl.make_partials(rows, P, D, seed=P * 7 + D, empty_frac=0.2 if P > 1 else 0.0)
+    m[0] = float("-inf")
+    l[0] = 0.0
+    acc[0] = 0.0  # a row with nothing visible
+    o = ef.combine(m.cuda(), l.cuda(), acc.cuda())
+    torch.cuda.synchronize()
+    o = o.cpu().double().numpy()
+    ref = oracle.combine_ref(m.numpy(), l.numpy(), acc.numpy())
+    scale = oracle.combine_error_scale(m.numpy(), l.numpy(), acc.numpy())
+    assert np.isfinite(o).all()
+    assert (np.abs(o - ref) <= COMBINE_REL * scale + 1e-30).all(), float(
+        np.max(np.abs(o - ref) / np.maximum(scale, 1e-30)))
+    assert (o[0] == 0).all()
+
+
+@pytest.mark.parametrize("shape", [(1, 8, 2, 1, 1000, 128, 256), (1, 16, 2, 4, 700, 128, 128),
+                                   (2, 4, 4, 1, 300, 64, 64)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_partial_states_match_oracle(shape):
+    """Stored states per partition: compare what is unique about a state, its
+    log-sum-exp m + ln(l) and its partial output acc / l (the reference point m
+    itself is free); empty partitions must be exactly the identity."""
+    B, Hq, Hkv, Sq, Skv, D, T = shape
+    announce(f"partials {shape}")
+    q, k, v = inputs(B, Hq, Hkv, Sq, Skv, D, seed=300 + Skv)
+    scale = 1.0 / math.sqrt(D)
+    qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+    ws = ef.make_workspace(qd, kd, T)
+    ef.attention_splitkv(qd, kd, vd, scale=scale, causal=True, partition_size=T, workspace=ws)
+    torch.cuda.synchronize()
+    m, l, acc = (x.cpu().double().numpy() for x in ef.workspace_views(ws, B, Hq, Sq, Skv, D, T))
+    rm, rl, racc = oracle.splitkv_partials_ref(f64(q), f64(k), f64(v), scale, True, T)
+    empty = np.isneginf(rm)
+    assert (np.isneginf(m) == empty).all()
+    assert (l[empty] == 0).all() and (acc[empty] == 0).all()
+    live = ~empty
+    lse, rlse = m[live] + np.log(l[live]), rm[live] + np.log(rl[live])
+    assert np.max(np.abs(lse - rlse)) <= 1e-3
+    po = acc[live] / l[live][:, None]
+    rpo = racc[live] / rl[live][:, None]
+    assert np.max(np.abs(po - rpo)) <= MAX_ABS and np.mean(np.abs(po - rpo)) <= MEAN_ABS
+
+
+# ---------------------------------------------------------------------------
+# Invariants of the HIP path itself.
+# ---------------------------------------------------------------------------
+
+
+def test_deterministic_and_fwd_matches_split():
+    announce("determinism")
+    q, k, v = inputs(2, 8, 2, 1, 3000, 128, seed=9)
+    q, k, v = q.cuda(), k.cuda(), v.cuda()
+    a = ef.attention_splitkv(q, k, v, causal=False, partition_size=256)
+    b = ef.attention_splitkv(q, k, v, causal=False, partition_size=256)
+    c = ef.attention_fwd(q, k, v, causal=False)
+    d = ef.attention_fwd(q, k, v, causal=False)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b) and torch.equal(c, d)
+    assert float((a - c).abs().max()) <= MAX_ABS
+    qp, kp, vp = inputs(1, 8, 2, 300, 300, 128, seed=10)
+    e = ef.attention_fwd(qp.cuda(), kp.cuda(), vp.cuda(), causal=True)
+    f = ef.attention_fwd(qp.cuda(), kp.cuda(), vp.cuda(), causal=True)
+    torch.cuda.synchronize()
+    assert torch.equal(e, f)
+
+
+@pytest.mark.parametrize("path", ["fwd", "splitkv"])
+def test_poisoned_output_fully_written_and_guard_band_intact(path):
+    announce(f"poison {path}")
+    B, Hq, Hkv, Sq, Skv, D = 1, 8, 2, 2, 500, 128
+    q, k, v = inputs(B, Hq, Hkv, Sq, Skv, D, seed=11)
+    n = B * Hq * Sq * D
+    buf = torch.full((n + 4096,), float("nan"), dtype=torch.float32, device="cuda")
+    buf[n:] = 12345.0
+    o = buf[:n].view(B, Hq, Sq, D)
+    qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+    if path == "fwd":
+        ef.attention_fwd(qd, kd, vd, causal=True, out=o)
+    else:
+        ws = ef.make_workspace(qd, kd, 64)
+        ws.fill_(255)  # NaN bit patterns everywhere
+        ef.attention_splitkv(qd, kd, vd, causal=True, partition_size=64, workspace=ws, out=o)
+    torch.cuda.synchronize()
+    assert torch.isfinite(o).all()
+    assert (buf[n:] == 12345.0).all()
+    ref = oracle.attention_ref(f64(q), f64(k), f64(v), 1 / math.sqrt(D), True)
+    assert_close(o, ref, f"poison {path}")
+
+
+def test_invalid_arguments_write_nothing():
+    announce("invalid args")
+    q, k, v = inputs(1, 4, 2, 4, 100, 128, seed=12)
+    q, k, v = q.cuda(), k.cuda(), v.cuda()
+    o = torch.full((1, 4, 4, 128), 7.0, device="cuda")
+    st = ef.ef_attention_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), 1, 4, 2, 4,
+                             100, 96, 0.1, 0, torch.cuda.current_stream().cuda_stream)
+    assert st == 4
+    ws = torch.zeros(16, dtype=torch.uint8, device="cuda")
+    st = ef.ef_attention_splitkv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), 1, 4, 2,
+                                 4, 100, 128, 0.1, 0, 64, ws.data_ptr(), 16,
+                                 torch.cuda.current_stream().cuda_stream)
+    assert st == 7
+    torch.cuda.synchronize()
+    assert (o == 7.0).all() and (ws == 0).all()
+
+
+def test_empty_inputs():
+    announce("empty inputs")
+    q = torch.zeros(1, 4, 3, 128, dtype=torch.bfloat16, device="cuda")
+    k = torch.zeros(1, 2, 0, 128, dtype=torch.bfloat16, device="cuda")
+    kk = torch.zeros(1, 2, 8, 128, dtype=torch.bfloat16, device="cuda")
+    o = torch.full((1, 4, 3, 128), 5.0, device="cuda")
+    ef.attention_fwd(q, k, k, out=o)
+    torch.cuda.synchronize()
+    assert (o == 0).all()
+    o.fill_(5.0)
+    ef.attention_splitkv(q, k, k, out=o, workspace=torch.zeros(256, dtype=torch.uint8,
+                                                                 device="cuda"))
+    torch.cuda.synchronize()
+    assert (o == 0).all()
+    q0 = torch.zeros(0, 4, 3, 128, dtype=torch.bfloat16, device="cuda")
+    k0 = torch.zeros(0, 2, 8, 128, dtype=torch.bfloat16, device="cuda")
+    assert ef.attention_fwd(q0, k0, k0).numel() == 0
+    # Sq > Skv with a causal mask: the first Sq - Skv rows see nothing
+    qq = torch.randn(1, 4, 10, 128, device="cuda").to(torch.bfloat16)
+    o = ef.attention_fwd(qq, kk, kk, causal=True)
+    torch.cuda.synchronize()
+    assert (o[:, :, :2] == 0).all() and torch.isfinite(o).all()
+
+
+def test_non_default_stream():
+    announce("stream")
+    q, k, v = inputs(1, 8, 2, 1, 2048, 128, seed=13)
+    q, k, v = q.cuda(), k.cuda(), v.cuda()
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        o = ef.attention_splitkv(q, k, v, partition_size=256)
+        o2 = ef.attention_fwd(q, k, v)
+    s.synchronize()
+    ref = oracle.attention_ref(f64(q.cpu()), f64(k.cpu()), f64(v.cpu()), 1 / math.sqrt(128), False)
+    assert_close(o, ref, "stream split")
+    assert_close(o2, ref, "stream fwd")
