@@ -68,29 +68,34 @@ struct Loader {
   static_assert(K_CHUNKS % NT == 0, "K tile split");
   static_assert(V_GROUPS % NT == 0 || NT % V_GROUPS == 0, "V tile split");
 
-  uint4 kreg[K_PER_T];
-  uint4 vreg[V_PER_T][4];
+  u32x4_t kreg[K_PER_T];
+  u32x4_t vreg[V_PER_T][4];
 
+  // Keys past the end of the range are clamped to the last valid key: the loads
+  // stay unconditional (no divergent branch, so the compiler does not have to wait
+  // for them before the compute that follows), the duplicated K rows are masked
+  // out of the scores and the duplicated V rows meet a weight of exactly 0.
   __device__ __forceinline__ void load(const uint16_t* kh, const uint16_t* vh, int kb, int kend) {
     const int t = threadIdx.x;
+    const int klast = kend - 1;
 #pragma unroll
     for (int i = 0; i < K_PER_T; ++i) {
       const int id = t + i * NT;
       const int row = id / G::KCH, ch = id % G::KCH;
-      const int key = kb + row;
-      kreg[i] = key < kend ? *reinterpret_cast<const uint4*>(kh + (size_t)key * D + ch * 8)
-                           : make_uint4(0u, 0u, 0u, 0u);
+      const int key = min(kb + row, klast);
+      kreg[i] = *reinterpret_cast<const u32x4_t*>(kh + (size_t)key * D + ch * 8);
     }
 #pragma unroll
     for (int i = 0; i < V_PER_T; ++i) {
       const int gid = t + i * NT;
       const int ch = gid % G::KCH, kq = gid / G::KCH;
-      if (gid >= V_GROUPS) break;
+      if constexpr (V_GROUPS % NT != 0) {
+        if (gid >= V_GROUPS) break;
+      }
 #pragma unroll
       for (int x = 0; x < 4; ++x) {
-        const int key = kb + kq * 4 + x;
-        vreg[i][x] = key < kend ? *reinterpret_cast<const uint4*>(vh + (size_t)key * D + ch * 8)
-                                : make_uint4(0u, 0u, 0u, 0u);
+        const int key = min(kb + kq * 4 + x, klast);
+        vreg[i][x] = *reinterpret_cast<const u32x4_t*>(vh + (size_t)key * D + ch * 8);
       }
     }
   }
@@ -103,37 +108,43 @@ struct Loader {
     for (int i = 0; i < K_PER_T; ++i) {
       const int id = t + i * NT;
       const int row = id / G::KCH, ch = id % G::KCH;
-      *reinterpret_cast<uint4*>(ks + row * (2 * D) + ((ch ^ swz_k(row, G::KCH)) << 4)) = kreg[i];
+      *reinterpret_cast<u32x4_t*>(ks + row * (2 * D) + ((ch ^ swz_k(row, G::KCH)) << 4)) = kreg[i];
     }
 #pragma unroll
     for (int i = 0; i < V_PER_T; ++i) {
       const int gid = t + i * NT;
       const int ch = gid % G::KCH, kq = gid / G::KCH;
-      if (gid >= V_GROUPS) break;
+      if constexpr (V_GROUPS % NT != 0) {
+        if (gid >= V_GROUPS) break;
+      }
       const int slot = vslot(kq * 4);
-      const uint32_t* x0 = reinterpret_cast<const uint32_t*>(&vreg[i][0]);
-      const uint32_t* x1 = reinterpret_cast<const uint32_t*>(&vreg[i][1]);
-      const uint32_t* x2 = reinterpret_cast<const uint32_t*>(&vreg[i][2]);
-      const uint32_t* x3 = reinterpret_cast<const uint32_t*>(&vreg[i][3]);
+      const u32x4_t x0 = vreg[i][0], x1 = vreg[i][1], x2 = vreg[i][2], x3 = vreg[i][3];
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
 #pragma unroll
         for (int half = 0; half < 2; ++half) {
           const uint32_t sel = half ? 0x07060302u : 0x05040100u;
-          uint2 val;
-          val.x = __builtin_amdgcn_perm(x1[w], x0[w], sel);  // keys 0,1 at d
-          val.y = __builtin_amdgcn_perm(x3[w], x2[w], sel);  // keys 2,3 at d
+          u32x2_t val;
+          val[0] = __builtin_amdgcn_perm(x1[w], x0[w], sel);  // keys 0,1 at d
+          val[1] = __builtin_amdgcn_perm(x3[w], x2[w], sel);  // keys 2,3 at d
           const int d = ch * 8 + w * 2 + half;
           const int chunk = (slot >> 3) ^ swz_v(d);
-          *reinterpret_cast<uint2*>(vs + d * (2 * BN) + (chunk << 4) + ((slot & 7) << 1)) = val;
+          *reinterpret_cast<u32x2_t*>(vs + d * (2 * BN) + (chunk << 4) + ((slot & 7) << 1)) = val;
         }
       }
     }
   }
 };
 
+// Occupancy target: two waves per SIMD for 4-wave workgroups (two workgroups per
+// CU overlap each other's barrier and memory stalls); the 2-wave variant keeps
+// its larger per-thread staging registers at one wave per SIMD.
+template <int NW>
+constexpr int kWavesPerEu = NW == 4 ? 2 : 1;
+
 template <int D, int NW, bool NEG>
-__global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(MfmaParams a) {
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(kWavesPerEu<NW>)))
+void attn_mfma_kernel(MfmaParams a) {
   using Geo = TileGeom<D>;
   constexpr int KSTEPS = D / 16;  // MFMA k-steps over the head dimension
   constexpr int DT = D / 32;      // 32-wide output tiles along D
@@ -181,10 +192,11 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(MfmaParams a) {
   // Q^T fragments (B operand): lane holds q[row][16*s + 8*h .. +8].
   bf16x8_t qf[KSTEPS];
   {
-    const uint4* qp = reinterpret_cast<const uint4*>(a.q + orow * D);
+    const u32x4_t* qp = reinterpret_cast<const u32x4_t*>(a.q + orow * D);
+    const u32x4_t zero = {0u, 0u, 0u, 0u};
 #pragma unroll
     for (int s = 0; s < KSTEPS; ++s) {
-      uint4 x = rvalid ? qp[2 * s + h] : make_uint4(0u, 0u, 0u, 0u);
+      u32x4_t x = rvalid ? qp[2 * s + h] : zero;
       qf[s] = __builtin_bit_cast(bf16x8_t, x);
     }
   }
@@ -209,7 +221,7 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(MfmaParams a) {
     const int kb = kbeg + j * BN;
     char* stage = smem + (j & 1) * Geo::STAGE;
     const bool more = j + 1 < ntiles;
-    if (more) ld.load(kh, vh, kb + BN, kend);
+    ld.load(kh, vh, kb + BN, kend);  // past the end: every key clamps to the last one
 
     // S^T = K * Q^T for two 32-key halves of the tile.
     floatx16 sacc[2];
@@ -222,7 +234,7 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(MfmaParams a) {
 #pragma unroll
       for (int s = 0; s < KSTEPS; ++s) {
         const int ch = 2 * s + h;
-        const uint4 kx = *reinterpret_cast<const uint4*>(
+        const u32x4_t kx = *reinterpret_cast<const u32x4_t*>(
             ks + krow * (2 * D) + ((ch ^ swz_k(krow, Geo::KCH)) << 4));
         sacc[half] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
             __builtin_bit_cast(bf16x8_t, kx), qf[s], sacc[half], 0, 0, 0);
@@ -279,13 +291,13 @@ __global__ __launch_bounds__(NW * 64) void attn_mfma_kernel(MfmaParams a) {
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       // P^T fragment: registers 8*(s%2) .. +8 of score half s/2, i.e. pk[4*s .. 4*s+3].
-      const uint4 pv = make_uint4(pk[4 * s], pk[4 * s + 1], pk[4 * s + 2], pk[4 * s + 3]);
+      const u32x4_t pv = {pk[4 * s], pk[4 * s + 1], pk[4 * s + 2], pk[4 * s + 3]};
       const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pv);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
         const int d = dt * 32 + ql;
         const int chunk = (2 * s + h) ^ swz_v(d);
-        const uint4 vx = *reinterpret_cast<const uint4*>(vs + d * (2 * BN) + (chunk << 4));
+        const u32x4_t vx = *reinterpret_cast<const u32x4_t*>(vs + d * (2 * BN) + (chunk << 4));
         oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vx), pf,
                                                           oacc[dt], 0, 0, 0);
       }

@@ -62,24 +62,32 @@ __global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
 
   const float c = a.c;  // scale * log2(e): scores are kept in base-2 units
   constexpr int STEP = NW * TPL;  // key rows per workgroup-wide load
+  // Rows past the partition are clamped to its last row: the loads stay
+  // unconditional and the duplicates are masked out of the scores. The rows of
+  // the next iteration are requested before the current ones are used.
+  const int tlast = t1 - 1;
+  uint4 kn[U], vn[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int t = min(t0 + (u * NW + wave) * TPL + tl, tlast);
+    kn[u] = load_nt16(kp + (size_t)t * LPR);
+    vn[u] = load_nt16(vp + (size_t)t * LPR);
+  }
   for (int tb = t0; tb < t1; tb += U * STEP) {
     uint4 kr[U], vr[U];
     int tok[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
+      kr[u] = kn[u];
+      vr[u] = vn[u];
       tok[u] = tb + (u * NW + wave) * TPL + tl;
-      if (tok[u] < t1) {
-        kr[u] = load_nt16(kp + (size_t)tok[u] * LPR);
-      } else {
-        kr[u] = make_uint4(0u, 0u, 0u, 0u);
-      }
     }
+    if (tb + U * STEP < t1) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      if (tok[u] < t1) {
-        vr[u] = load_nt16(vp + (size_t)tok[u] * LPR);
-      } else {
-        vr[u] = make_uint4(0u, 0u, 0u, 0u);
+      for (int u = 0; u < U; ++u) {
+        const int t = min(tb + U * STEP + (u * NW + wave) * TPL + tl, tlast);
+        kn[u] = load_nt16(kp + (size_t)t * LPR);
+        vn[u] = load_nt16(vp + (size_t)t * LPR);
       }
     }
     // Scores in base-2 units, masked to -inf where the key is not visible.

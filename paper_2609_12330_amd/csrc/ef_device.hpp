@@ -18,6 +18,7 @@ constexpr float kLn2 = 0.6931471805599453f;
 constexpr float kNegInf = -__builtin_inff();
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 // 16-byte global load marked non-temporal (streamed once, not kept in cache).
 __device__ __forceinline__ uint4 load_nt16(const uint4* p) {
