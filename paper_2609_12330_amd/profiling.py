@@ -1,0 +1,155 @@
+"""Summaries of rocprofv3 runs of bench.py, for the files under profiles/.
+
+Two inputs are read, both rocprofv3 CSV output (``-f csv``):
+
+* ``<prefix>_kernel_stats.csv`` of a ``--kernel-trace --stats`` run: per
+  kernel name, the number of dispatches and their average duration;
+* ``<prefix>_counter_collection.csv`` of two ``--pmc FETCH_SIZE`` and
+  ``--pmc WRITE_SIZE`` runs of ``bench.py --calibrate-copy``: per dispatch,
+  the HBM bytes the L2 read and wrote, in KiB. The same runs include a plain
+  device copy of known size (256 MiB), and each counter is scaled by the ratio
+  of that copy's true bytes to what the counter reports for it.
+
+    python -m paper_2609_12330_amd.profiling \\
+        --stats k_kernel_stats.csv --fetch f_counter_collection.csv \\
+        --write w_counter_collection.csv --kernel decode_split_kernel \\
+        --workload gqa_decode_b8_h32x8_kv4096_d128 --sources decode_split.hip ef_device.hpp \\
+        --algorithmic-bytes 134283264 --command "..." --out-prefix profiles/decode_split_...
+"""
+
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import json
+import os
+from collections import defaultdict
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+CSRC = os.path.join(PKG, "csrc")
+COPY_BYTES = 256 << 20
+COPY_KERNEL_MARKERS = ("copyBuffer",)
+
+
+def source_hash(*names) -> str:
+    """Short hash of kernel sources; counter data is valid only for the hashed sources."""
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(CSRC, n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def kernel_stats(path):
+    out = []
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            out.append({"name": r["Name"], "calls": int(r["Calls"]),
+                        "avg_us": float(r["AverageNs"]) / 1e3, "min_us": float(r["MinNs"]) / 1e3,
+                        "max_us": float(r["MaxNs"]) / 1e3, "pct": float(r["Percentage"])})
+    return out
+
+
+def counter_means(path):
+    """Mean counter value per (kernel name, counter) over dispatches."""
+    acc = defaultdict(list)
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            acc[(r["Kernel_Name"], r["Counter_Name"])].append(float(r["Counter_Value"]))
+    return {k: (sum(v) / len(v), len(v)) for k, v in acc.items()}
+
+
+def _pick(means, counter, pred):
+    hits = [(k[0], v) for k, v in means.items() if k[1] == counter and pred(k[0])]
+    if not hits:
+        raise ValueError(f"no dispatch of a matching kernel carries {counter}")
+    return hits[0]
+
+
+def traffic(fetch_csv, write_csv, kernel_substr):
+    """HBM bytes per dispatch of the kernel, each counter scaled by the copy calibration."""
+    f = counter_means(fetch_csv)
+    w = counter_means(write_csv)
+    is_copy = lambda n: any(m in n for m in COPY_KERNEL_MARKERS)  # noqa: E731
+    is_kernel = lambda n: kernel_substr in n  # noqa: E731
+    _, (copy_fetch, _) = _pick(f, "FETCH_SIZE", is_copy)
+    _, (copy_write, _) = _pick(w, "WRITE_SIZE", is_copy)
+    kname, (k_fetch, n_f) = _pick(f, "FETCH_SIZE", is_kernel)
+    _, (k_write, n_w) = _pick(w, "WRITE_SIZE", is_kernel)
+    fetch_factor = COPY_BYTES / (copy_fetch * 1024.0)
+    write_factor = COPY_BYTES / (copy_write * 1024.0)
+    fetch_b = k_fetch * 1024.0 * fetch_factor
+    write_b = k_write * 1024.0 * write_factor
+    return {
+        "kernel": kname,
+        "dispatches": {"fetch": n_f, "write": n_w},
+        "fetch_size_kib_raw": k_fetch,
+        "write_size_kib_raw": k_write,
+        "copy_calibration": {"copy_bytes": COPY_BYTES, "fetch_size_kib": copy_fetch,
+                             "write_size_kib": copy_write, "fetch_factor": fetch_factor,
+                             "write_factor": write_factor},
+        "hbm_fetch_bytes_per_launch": fetch_b,
+        "hbm_write_bytes_per_launch": write_b,
+        "hbm_bytes_per_launch": fetch_b + write_b,
+    }
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--stats", required=True)
+    ap.add_argument("--fetch")
+    ap.add_argument("--write")
+    ap.add_argument("--kernel", required=True, help="substring of the dominant kernel's name")
+    ap.add_argument("--workload", required=True)
+    ap.add_argument("--sources", nargs="+", required=True)
+    ap.add_argument("--algorithmic-bytes", type=float, default=None)
+    ap.add_argument("--command", required=True, help="the rocprofv3 command lines that were run")
+    ap.add_argument("--bench-line", default=None, help="file holding the bench JSON line")
+    ap.add_argument("--out-prefix", required=True)
+    a = ap.parse_args()
+
+    stats = kernel_stats(a.stats)
+    lines = [f"# {a.kernel} on {a.workload}", "", "Commands (from the repository root on the GPU "
+             "box, `cd /tmp && export TMPDIR=/tmp` first):", "", "```", a.command, "```", "",
+             "## rocprofv3 --kernel-trace --stats", "",
+             "| kernel | calls | avg us | min us | max us | % time |", "|---|---|---|---|---|---|"]
+    for s in stats:
+        lines.append(f"| `{s['name']}` | {s['calls']} | {s['avg_us']:.2f} | {s['min_us']:.2f} | "
+                     f"{s['max_us']:.2f} | {s['pct']:.1f} |")
+    if a.fetch and a.write:
+        t = traffic(a.fetch, a.write, a.kernel)
+        t["source_hash"] = source_hash(*a.sources)
+        t["sources"] = a.sources
+        t["workload"] = a.workload
+        if a.algorithmic_bytes:
+            t["algorithmic_bytes_per_launch"] = a.algorithmic_bytes
+            t["traffic_over_algorithmic"] = t["hbm_bytes_per_launch"] / a.algorithmic_bytes
+        c = t["copy_calibration"]
+        lines += ["", "## HBM traffic (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE)", "",
+                  f"Calibration: a {c['copy_bytes']} B device copy reads FETCH_SIZE "
+                  f"{c['fetch_size_kib']:.0f} KiB and WRITE_SIZE {c['write_size_kib']:.0f} KiB, "
+                  f"so FETCH_SIZE is scaled by {c['fetch_factor']:.3f} and WRITE_SIZE by "
+                  f"{c['write_factor']:.3f}.", "",
+                  f"`{t['kernel']}`: FETCH_SIZE {t['fetch_size_kib_raw']:.1f} KiB, WRITE_SIZE "
+                  f"{t['write_size_kib_raw']:.1f} KiB per dispatch -> "
+                  f"{t['hbm_fetch_bytes_per_launch'] / 1e6:.2f} MB read + "
+                  f"{t['hbm_write_bytes_per_launch'] / 1e6:.2f} MB written = "
+                  f"{t['hbm_bytes_per_launch'] / 1e6:.2f} MB per launch"
+                  + (f" ({t['traffic_over_algorithmic']:.3f} x the algorithmic "
+                     f"{a.algorithmic_bytes / 1e6:.2f} MB)." if a.algorithmic_bytes else "."),
+                  "", f"Source hash of {', '.join(a.sources)}: `{t['source_hash']}`."]
+        with open(a.out_prefix + "_traffic.json", "w") as f:
+            json.dump(t, f, indent=1)
+    if a.bench_line:
+        with open(a.bench_line) as f:
+            js = [ln for ln in f if ln.startswith("{")]
+        if js:
+            lines += ["", "## bench.py line of the kernel-trace run", "", "```", js[-1].strip(),
+                      "```"]
+    with open(a.out_prefix + ".md", "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+if __name__ == "__main__":
+    main()
