@@ -8,6 +8,8 @@ into o. The default workload is grouped-query decode, B=8, Hq=32, Hkv=8,
 Sq=1, Skv=4096, D=128, 256-key partitions; the metric is KV bytes read per
 second over the whole step. K/V inputs rotate over enough buffer sets that
 no step finds its K/V in the 256 MB last-level cache left by the step before.
+The K timed steps are captured in one HIP graph and replayed, so host launch
+cost stays out of the figure (the paper times under CUDA Graphs).
 
 Prints one JSON line. `--config` selects another workload (the causal prefill
 is reported in TFLOP/s through ef_attention_fwd).
@@ -134,7 +136,6 @@ def main():
         sets.append((q.to(dev), k.to(dev), v.to(dev)))
     o = torch.empty(cfg.B, cfg.Hq, cfg.Sq, cfg.D, dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
-    sh = stream.cuda_stream
     B, Hq, Hkv, Sq, Skv, D = cfg.B, cfg.Hq, cfg.Hkv, cfg.Sq, cfg.Skv, cfg.D
 
     if decode:
@@ -147,27 +148,46 @@ def main():
 
         def produce(i):
             q, k, v = sets[i % nbuf]
+            sh = torch.cuda.current_stream().cuda_stream
             st = ef.ef_attention_splitkv_partials(q.data_ptr(), k.data_ptr(), v.data_ptr(), B, Hq,
                                                   Hkv, Sq, Skv, D, cfg.scale, cfg.causal, T,
                                                   ws.data_ptr(), wsb, sh)
             if st:
                 raise RuntimeError(f"library error {st}")
 
+        # The library runs the combine inside the producer when G*Sq <= 8 and P <= 64;
+        # otherwise the producer is followed by a separate combine kernel.
+        fused = cfg.G * Sq <= 8 and P <= 64
+
         def step(i, ev=None):
             q, k, v = sets[i % nbuf]
+            cur = torch.cuda.current_stream()
+            sh = cur.cuda_stream
             if ev is not None:
-                ev[0].record(stream)
-            st = ef.ef_attention_splitkv_partials(q.data_ptr(), k.data_ptr(), v.data_ptr(), B, Hq,
-                                                  Hkv, Sq, Skv, D, cfg.scale, cfg.causal, T,
-                                                  ws.data_ptr(), wsb, sh)
-            if ev is not None:
-                ev[1].record(stream)
-            st |= ef.ef_attention_combine(m.data_ptr(), l.data_ptr(), acc.data_ptr(), o.data_ptr(),
-                                          rows, P, D, sh)
-            if ev is not None:
-                ev[2].record(stream)
+                ev[0].record(cur)
+            if fused:
+                st = ef.ef_attention_splitkv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                             B, Hq, Hkv, Sq, Skv, D, cfg.scale, cfg.causal, T,
+                                             ws.data_ptr(), wsb, sh)
+                if ev is not None:
+                    ev[1].record(cur)
+                    ev[2].record(cur)
+            else:
+                st = ef.ef_attention_splitkv_partials(q.data_ptr(), k.data_ptr(), v.data_ptr(), B,
+                                                      Hq, Hkv, Sq, Skv, D, cfg.scale, cfg.causal,
+                                                      T, ws.data_ptr(), wsb, sh)
+                if ev is not None:
+                    ev[1].record(cur)
+                st |= ef.ef_attention_combine(m.data_ptr(), l.data_ptr(), acc.data_ptr(),
+                                              o.data_ptr(), rows, P, D, sh)
+                if ev is not None:
+                    ev[2].record(cur)
             if st:
                 raise RuntimeError(f"library error {st}")
+
+        if fused:
+            def produce(i):  # noqa: F811  (one kernel: producer with the combine inside)
+                step(i)
     else:
         T, P = Skv, 1
 
@@ -176,13 +196,14 @@ def main():
 
         def step(i, ev=None):
             q, k, v = sets[i % nbuf]
+            cur = torch.cuda.current_stream()
             if ev is not None:
-                ev[0].record(stream)
+                ev[0].record(cur)
             st = ef.ef_attention_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B, Hq,
-                                     Hkv, Sq, Skv, D, cfg.scale, cfg.causal, sh)
+                                     Hkv, Sq, Skv, D, cfg.scale, cfg.causal, cur.cuda_stream)
             if ev is not None:
-                ev[1].record(stream)
-                ev[2].record(stream)
+                ev[1].record(cur)
+                ev[2].record(cur)
             if st:
                 raise RuntimeError(f"library error {st}")
 
@@ -192,13 +213,19 @@ def main():
     print(f"[bench] {cfg.name}: warmup done ({args.warmup} steps, {nbuf} buffer sets)",
           file=sys.stderr, flush=True)
 
-    # Timed region: K whole steps back to back, nothing else on the stream.
-    t_beg, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    # Timed region: K whole steps back to back, replayed from a HIP graph so the
+    # host's launch cost is not in the figure (the paper times under CUDA Graphs).
+    # The graph is replayed once untimed before the timed replay.
+    g_steps = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_steps):
+        for i in range(args.steps):
+            step(args.warmup + i)
+    g_steps.replay()
     torch.cuda.synchronize()
+    t_beg, t_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     t0 = time.perf_counter()
     t_beg.record(stream)
-    for i in range(args.steps):
-        step(args.warmup + i)
+    g_steps.replay()
     t_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -206,13 +233,18 @@ def main():
     ev_ms_step = t_beg.elapsed_time(t_end) / args.steps
 
     # Kernel timing on the same stream: the dominant (producer) kernel launched
-    # back to back over the same rotating buffer sets, HIP events at both ends,
-    # and once more with an event pair around every launch.
+    # back to back from a graph over the same rotating buffer sets, HIP events at
+    # both ends; and eagerly with an event pair around every launch.
     n_k = max(args.steps, 20)
+    g_prod = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g_prod):
+        for i in range(n_k):
+            produce(i)
+    g_prod.replay()
+    torch.cuda.synchronize()
     k_beg, k_end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     k_beg.record(stream)
-    for i in range(n_k):
-        produce(i)
+    g_prod.replay()
     k_end.record(stream)
     torch.cuda.synchronize()
     prod_avg = k_beg.elapsed_time(k_end) / n_k
@@ -239,10 +271,12 @@ def main():
     q_bytes = B * Hq * Sq * D * 2
     if decode:
         # Producer: algorithmic bytes = bf16 q + K + V read once (512 B per key per kv head).
-        kernel = "decode_split" if cfg.Sq * cfg.G <= 8 else "attn_mfma_split"
-        src = source_hash("decode_split.hip" if kernel == "decode_split" else "attn_mfma.hip",
-                          "ef_device.hpp")
-        alg = kv + q_bytes
+        kernel = ("decode_split" if cfg.Sq * cfg.G <= 8 else "attn_mfma_split") + (
+            "_fused" if fused else "")
+        src = source_hash(*(("decode_split.hip", "group_combine.hpp") if cfg.Sq * cfg.G <= 8
+                            else ("attn_mfma.hip",)), "ef_device.hpp")
+        # fused: q, K, V read and o written by the one kernel; else the producer reads q, K, V
+        alg = cfg.algorithmic_bytes() if fused else kv + q_bytes
         achieved = alg / (prod_avg * 1e-3) / 1e9
         traffic = load_traffic(f"{kernel}_{cfg.name}", src, 1)
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,

@@ -96,12 +96,14 @@ int ef_attention_splitkv_partition_size(int B, int Hq, int Hkv, int Sq, int Skv,
  *     m   [rows][P]    fp32 at byte 0
  *     l   [rows][P]    fp32 at byte  A = round_up(rows*P*4, 256)
  *     acc [rows][P][D] fp32 at byte 2*A
+ *     counters [B*Hkv] uint32 at byte C = round_up(2*A + rows*P*D*4, 256)
  * with row = (b*Hq + hq)*Sq + sq: a reference point m for the scaled scores
  * s of the row's visible keys in partition p (natural-log units; at most the
  * partition maximum and within 8*ln(2) of it), l = sum exp(s - m) and
  * acc = sum exp(s - m) * v. (m, l, acc) and (m', l*e^(m-m'), acc*e^(m-m'))
  * describe the same state. A partition with no visible key holds the reducer
- * identity (-inf, 0, 0).
+ * identity (-inf, 0, 0). The counters are arrival counters of the fused
+ * combine (see ef_attention_splitkv).
  */
 size_t ef_attention_splitkv_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
                                            int partition_size);
@@ -121,7 +123,16 @@ size_t ef_attention_splitkv_workspace_size(int B, int Hq, int Hkv, int Sq, int S
  *                      ef_attention_splitkv_workspace_size(...) bytes,
  *                      16-byte aligned; on return (stream-ordered) it holds
  *                      the partial states in the layout documented there.
+ *                      Its counter region must be zero before the first call
+ *                      that uses it (zero-fill the new buffer once); every
+ *                      call leaves it zero again, so a workspace serves any
+ *                      number of calls in stream order. Calls that overlap
+ *                      in time must not share a workspace.
  *   workspace_bytes  : its size in bytes.
+ * When G*Sq <= 8 and P <= 64 the combine runs inside the producer: the last
+ * workgroup of each (batch, kv head) to store its state, found with the
+ * group's arrival counter, combines that group's rows and resets the counter
+ * (one kernel instead of two). Otherwise a separate combine kernel follows.
  * Other arguments as for ef_attention_fwd.
  */
 ef_status ef_attention_splitkv(const void* q, const void* k, const void* v, float* o,

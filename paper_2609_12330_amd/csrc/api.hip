@@ -58,16 +58,17 @@ int resolve_partition(const Shape& s, int partition_size) {
 }
 
 struct WsLayout {
-  size_t m_off, l_off, acc_off, bytes;
+  size_t m_off, l_off, acc_off, cnt_off, bytes;
 };
 
-WsLayout ws_layout(long long rows, long long P, int D) {
+WsLayout ws_layout(long long rows, long long P, int D, long long kv_heads) {
   WsLayout w;
   const size_t a = ef::ws_align256((size_t)(rows * P) * sizeof(float));
   w.m_off = 0;
   w.l_off = a;
   w.acc_off = 2 * a;
-  w.bytes = 2 * a + (size_t)(rows * P) * (size_t)D * sizeof(float);
+  w.cnt_off = ef::ws_align256(2 * a + (size_t)(rows * P) * (size_t)D * sizeof(float));
+  w.bytes = w.cnt_off + (size_t)kv_heads * sizeof(unsigned);
   return w;
 }
 
@@ -148,7 +149,7 @@ size_t ef_attention_splitkv_workspace_size(int B, int Hq, int Hkv, int Sq, int S
   if (s.rows() == 0 || Skv == 0) return 0;
   const int T = resolve_partition(s, partition_size);
   const long long P = (Skv + (long long)T - 1) / T;
-  return ws_layout(s.rows(), P, D).bytes;
+  return ws_layout(s.rows(), P, D, (long long)B * Hkv).bytes;
 }
 
 }  // extern "C"
@@ -160,7 +161,7 @@ namespace {
 ef_status split_prepare(const Shape& s, const void* q, const void* k, const void* v,
                         const float* o, float scale, int partition_size, void* workspace,
                         size_t workspace_bytes, int* T_out, int* P_out, float** ws_m,
-                        float** ws_l, float** ws_acc) {
+                        float** ws_l, float** ws_acc, unsigned** counters) {
   ef_status st = check_shape(s);
   if (st != EF_OK) return st;
   if (partition_size < 0 || partition_size % kTileKeys != 0) return EF_ERR_INVALID_PARTITION;
@@ -172,21 +173,24 @@ ef_status split_prepare(const Shape& s, const void* q, const void* k, const void
   const int T = resolve_partition(s, partition_size);
   const long long P = (s.Skv + (long long)T - 1) / T;
   if (P > kMaxGridYZ) return EF_ERR_INVALID_PARTITION;
-  const WsLayout w = ws_layout(s.rows(), P, s.D);
+  const WsLayout w = ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv);
   if (workspace == nullptr || workspace_bytes < w.bytes) return EF_ERR_WORKSPACE_TOO_SMALL;
   if (misaligned(workspace)) return EF_ERR_MISALIGNED;
   char* ws = static_cast<char*>(workspace);
   *ws_m = reinterpret_cast<float*>(ws + w.m_off);
   *ws_l = reinterpret_cast<float*>(ws + w.l_off);
   *ws_acc = reinterpret_cast<float*>(ws + w.acc_off);
+  *counters = reinterpret_cast<unsigned*>(ws + w.cnt_off);
   *T_out = T;
   *P_out = (int)P;
   return EF_OK;
 }
 
+// Stores the partition states; with `counters` and `o` given (decode path only),
+// the last workgroup of each (batch, kv head) also combines them into o.
 ef_status split_produce(const Shape& s, const void* q, const void* k, const void* v, float scale,
                         int causal, int T, int P, float* ws_m, float* ws_l, float* ws_acc,
-                        hipStream_t hs) {
+                        unsigned* counters, float* o, hipStream_t hs) {
   const int G = s.Hq / s.Hkv;
   const int R = G * s.Sq;
   if (R <= kDecodeMaxRows) {
@@ -204,6 +208,8 @@ ef_status split_produce(const Shape& s, const void* q, const void* k, const void
     a.P = P;
     a.c = scale * ef::kLog2e;
     a.causal = causal ? 1 : 0;
+    a.counters = counters;
+    a.o = o;
     return from_hip(ef::launch_decode_split(a, hs));
   }
   return launch_mfma(s, q, k, v, nullptr, ws_m, ws_l, ws_acc, T, P, scale, causal, hs);
@@ -220,11 +226,13 @@ ef_status ef_attention_splitkv_partials(const void* q, const void* k, const void
   const Shape s{B, Hq, Hkv, Sq, Skv, D};
   int T = 0, P = 0;
   float *ws_m = nullptr, *ws_l = nullptr, *ws_acc = nullptr;
+  unsigned* counters = nullptr;
   // The output pointer is not used here; pass q so the shared check sees a non-null pointer.
   ef_status st = split_prepare(s, q, k, v, static_cast<const float*>(q), scale, partition_size,
-                               workspace, workspace_bytes, &T, &P, &ws_m, &ws_l, &ws_acc);
+                               workspace, workspace_bytes, &T, &P, &ws_m, &ws_l, &ws_acc,
+                               &counters);
   if (st != EF_OK || P == 0) return st;
-  return split_produce(s, q, k, v, scale, causal, T, P, ws_m, ws_l, ws_acc,
+  return split_produce(s, q, k, v, scale, causal, T, P, ws_m, ws_l, ws_acc, nullptr, nullptr,
                        static_cast<hipStream_t>(stream));
 }
 
@@ -235,12 +243,16 @@ ef_status ef_attention_splitkv(const void* q, const void* k, const void* v, floa
   const Shape s{B, Hq, Hkv, Sq, Skv, D};
   int T = 0, P = 0;
   float *ws_m = nullptr, *ws_l = nullptr, *ws_acc = nullptr;
+  unsigned* counters = nullptr;
   ef_status st = split_prepare(s, q, k, v, o, scale, partition_size, workspace, workspace_bytes,
-                               &T, &P, &ws_m, &ws_l, &ws_acc);
+                               &T, &P, &ws_m, &ws_l, &ws_acc, &counters);
   if (st != EF_OK || s.rows() == 0) return st;
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (Skv == 0) return from_hip(ef::launch_zero_fill(o, (size_t)s.rows() * D, hs));
-  st = split_produce(s, q, k, v, scale, causal, T, P, ws_m, ws_l, ws_acc, hs);
+  const bool fused = (Hq / Hkv) * Sq <= kDecodeMaxRows && P <= ef::kFusedMaxP;
+  if (fused)
+    return split_produce(s, q, k, v, scale, causal, T, P, ws_m, ws_l, ws_acc, counters, o, hs);
+  st = split_produce(s, q, k, v, scale, causal, T, P, ws_m, ws_l, ws_acc, nullptr, nullptr, hs);
   if (st != EF_OK) return st;
   ef::CombineParams c{};
   c.m = ws_m;

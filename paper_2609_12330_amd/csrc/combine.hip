@@ -2,87 +2,133 @@
 // with h(c, s, s') = c * exp(s - s'), applied to the states that the producer
 // stored along the partition axis, section 3.3 "Collection").
 //
-// One workgroup of 4 waves per output row. Pass 1 takes M = max_p m_p over
-// the row's P partitions. Pass 2 lets wave w visit partitions w, w+4, ...,
-// weight each state by exp(m_p - M) (0 for the identity state m_p = -inf) and
-// accumulate the weighted acc (each lane owns D/64 adjacent elements) and the
-// weighted l; two accumulators per wave alternate over partitions to keep
-// the summation chains short. The four waves meet in LDS, in a fixed order,
-// so the result is deterministic.
+// Two layouts. With few partitions (P <= 32) one wave takes a whole row, each
+// lane owning D/64 adjacent elements and folding the partitions in order. With
+// many partitions, one wave takes a (row, 8-element slice of D): lane l takes partitions
+// p = l/2, l/2 + 32, ... and one 4-float half of the slice, so each pass of the
+// wave reads 32 partitions x 32 contiguous bytes and every lane keeps several
+// independent loads in flight. Each lane folds its partitions into one state
+// with the same reducer (reference moves up to the larger maximum, the other
+// side is rescaled by exp of the difference; the identity state (-inf, 0, 0)
+// contributes nothing), then the 32 partition lanes of each half merge
+// pairwise in a fixed butterfly order, so the result is deterministic.
 #include "ef_device.hpp"
 #include "ef_kernels.hpp"
 
 namespace ef {
 
+namespace {
+
+constexpr int kSlice = 8;              // floats of D per wave
+constexpr int kLanesPerPart = kSlice / 4;  // lanes per partition (one float4 each)
+constexpr int kPartsPerPass = 64 / kLanesPerPart;
+constexpr int kRowsKernelMaxP = 32;  // up to this many partitions: one wave per row
+
+struct Acc4 {
+  float m, l, a0, a1, a2, a3;
+};
+
+// Fold state (mb, lb, xb) into (s.m, s.l, s.a): rolling reducer on two states.
+__device__ __forceinline__ void fold(Acc4& s, float mb, float lb, float b0, float b1, float b2,
+                                     float b3) {
+  const float mn = fmaxf(s.m, mb);
+  const float ref = (mn == kNegInf) ? 0.f : mn;
+  const float wa = exp2_fast((s.m - ref) * kLog2e);  // 0 for the identity
+  const float wb = exp2_fast((mb - ref) * kLog2e);
+  s.l = s.l * wa + lb * wb;
+  s.a0 = s.a0 * wa + b0 * wb;
+  s.a1 = s.a1 * wa + b1 * wb;
+  s.a2 = s.a2 * wa + b2 * wb;
+  s.a3 = s.a3 * wa + b3 * wb;
+  s.m = mn;
+}
+
+}  // namespace
+
+// Many partitions: one wave per (row, 8-float slice).
+__global__ __launch_bounds__(64) void combine_sliced_kernel(CombineParams a) {
+  const int lane = threadIdx.x;
+  const int slices = a.D / kSlice;
+  const int row = blockIdx.x / slices;
+  const int slice = blockIdx.x % slices;
+  const int P = a.P;
+  const int half = lane % kLanesPerPart;
+  const int p0 = lane / kLanesPerPart;
+  const float* mrow = a.m + (size_t)row * P;
+  const float* lrow = a.l + (size_t)row * P;
+  const float* arow = a.acc + (size_t)row * P * a.D + slice * kSlice + half * 4;
+
+  Acc4 s{kNegInf, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int p = p0; p < P; p += kPartsPerPass) {
+    const float mp = mrow[p];
+    const float lp = lrow[p];
+    const float4 x = *reinterpret_cast<const float4*>(arow + (size_t)p * a.D);
+    fold(s, mp, lp, x.x, x.y, x.z, x.w);
+  }
+#pragma unroll
+  for (int off = kLanesPerPart; off < 64; off <<= 1) {
+    const float mb = shfl_xor(s.m, off), lb = shfl_xor(s.l, off);
+    const float b0 = shfl_xor(s.a0, off), b1 = shfl_xor(s.a1, off);
+    const float b2 = shfl_xor(s.a2, off), b3 = shfl_xor(s.a3, off);
+    fold(s, mb, lb, b0, b1, b2, b3);
+  }
+  if (lane < kLanesPerPart) {
+    const bool empty = s.m == kNegInf || s.l == 0.f;
+    const float inv = empty ? 0.f : 1.f / s.l;
+    float4 out = make_float4(s.a0 * inv, s.a1 * inv, s.a2 * inv, s.a3 * inv);
+    *reinterpret_cast<float4*>(a.o + (size_t)row * a.D + slice * kSlice + half * 4) = out;
+  }
+}
+
+// Few partitions: one wave per row, each lane owning D/64 adjacent elements and
+// folding the row's partitions in order.
 template <int D>
-__global__ __launch_bounds__(256) void combine_kernel(CombineParams a) {
-  constexpr int NW = 4;
-  constexpr int EPL = D / 64;  // elements per lane
-  const int row = blockIdx.x;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+__global__ __launch_bounds__(256) void combine_rows_kernel(CombineParams a) {
+  constexpr int EPL = D / 64;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= a.rows) return;
+  const int lane = threadIdx.x & 63;
   const int P = a.P;
   const float* mrow = a.m + (size_t)row * P;
   const float* lrow = a.l + (size_t)row * P;
-  const float* arow = a.acc + (size_t)row * P * D;
-
-  __shared__ float red[NW];
-  __shared__ float lsum[NW];
-  __shared__ float asum[NW][D];
-
-  float mx = kNegInf;
-  for (int p = threadIdx.x; p < P; p += NW * 64) mx = fmaxf(mx, mrow[p]);
+  const float* arow = a.acc + (size_t)row * P * D + lane * EPL;
+  float M = kNegInf, L = 0.f, A[EPL];
 #pragma unroll
-  for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, shfl_xor(mx, off));
-  if (lane == 0) red[wave] = mx;
-  __syncthreads();
-  float M = red[0];
+  for (int e = 0; e < EPL; ++e) A[e] = 0.f;
+#pragma unroll 4
+  for (int p = 0; p < P; ++p) {
+    const float mp = mrow[p];
+    const float lp = lrow[p];
+    float x[EPL];
 #pragma unroll
-  for (int w = 1; w < NW; ++w) M = fmaxf(M, red[w]);
-  const float Ms = (M == kNegInf) ? 0.f : M;
-
-  float A0[EPL], A1[EPL];
-  float L0 = 0.f, L1 = 0.f;
+    for (int e = 0; e < EPL; ++e) x[e] = arow[(size_t)p * D + e];
+    const float mn = fmaxf(M, mp);
+    const float ref = (mn == kNegInf) ? 0.f : mn;
+    const float wa = exp2_fast((M - ref) * kLog2e);
+    const float wb = exp2_fast((mp - ref) * kLog2e);
+    L = L * wa + lp * wb;
 #pragma unroll
-  for (int e = 0; e < EPL; ++e) A0[e] = A1[e] = 0.f;
-  int p = wave;
-  for (; p + NW < P; p += 2 * NW) {
-    const float w0 = exp2_fast((mrow[p] - Ms) * kLog2e);
-    const float w1 = exp2_fast((mrow[p + NW] - Ms) * kLog2e);
-    L0 = fmaf(w0, lrow[p], L0);
-    L1 = fmaf(w1, lrow[p + NW], L1);
-    const float* x0 = arow + (size_t)p * D + lane * EPL;
-    const float* x1 = arow + (size_t)(p + NW) * D + lane * EPL;
-#pragma unroll
-    for (int e = 0; e < EPL; ++e) {
-      A0[e] = fmaf(w0, x0[e], A0[e]);
-      A1[e] = fmaf(w1, x1[e], A1[e]);
-    }
+    for (int e = 0; e < EPL; ++e) A[e] = A[e] * wa + x[e] * wb;
+    M = mn;
   }
-  if (p < P) {
-    const float w0 = exp2_fast((mrow[p] - Ms) * kLog2e);
-    L0 = fmaf(w0, lrow[p], L0);
-    const float* x0 = arow + (size_t)p * D + lane * EPL;
+  const float inv = (M == kNegInf || L == 0.f) ? 0.f : 1.f / L;
 #pragma unroll
-    for (int e = 0; e < EPL; ++e) A0[e] = fmaf(w0, x0[e], A0[e]);
-  }
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) asum[wave][lane * EPL + e] = A0[e] + A1[e];
-  if (lane == 0) lsum[wave] = L0 + L1;
-  __syncthreads();
-  if (threadIdx.x < D) {
-    const int d = threadIdx.x;
-    const float L = (lsum[0] + lsum[1]) + (lsum[2] + lsum[3]);
-    const float S = (asum[0][d] + asum[1][d]) + (asum[2][d] + asum[3][d]);
-    a.o[(size_t)row * D + d] = (M == kNegInf || L == 0.f) ? 0.f : S / L;
-  }
+  for (int e = 0; e < EPL; ++e) a.o[(size_t)row * D + lane * EPL + e] = A[e] * inv;
 }
 
 hipError_t launch_combine(const CombineParams& a, hipStream_t stream) {
   if (a.rows == 0) return hipSuccess;
-  if (a.D == 128) {
-    hipLaunchKernelGGL(combine_kernel<128>, dim3(a.rows), dim3(256), 0, stream, a);
+  if (a.P <= kRowsKernelMaxP) {
+    const unsigned blocks = (unsigned)((a.rows + 3) / 4);
+    if (a.D == 128) {
+      hipLaunchKernelGGL(combine_rows_kernel<128>, dim3(blocks), dim3(256), 0, stream, a);
+    } else {
+      hipLaunchKernelGGL(combine_rows_kernel<64>, dim3(blocks), dim3(256), 0, stream, a);
+    }
   } else {
-    hipLaunchKernelGGL(combine_kernel<64>, dim3(a.rows), dim3(256), 0, stream, a);
+    const size_t waves = (size_t)a.rows * (a.D / kSlice);
+    hipLaunchKernelGGL(combine_sliced_kernel, dim3((unsigned)waves), dim3(64), 0, stream, a);
   }
   return hipGetLastError();
 }

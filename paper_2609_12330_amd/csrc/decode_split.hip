@@ -17,10 +17,11 @@
 // merged with the same reducer at the end.
 #include "ef_device.hpp"
 #include "ef_kernels.hpp"
+#include "group_combine.hpp"
 
 namespace ef {
 
-template <int D, int RMAX, int NW, int U>
+template <int D, int RMAX, int NW, int U, bool PF, bool NT = true, bool FUSED = false>
 __global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
   constexpr int LPR = D / 8;     // lanes per key row
   constexpr int TPL = 64 / LPR;  // key rows per wave-wide load
@@ -67,27 +68,36 @@ __global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
   // the next iteration are requested before the current ones are used.
   const int tlast = t1 - 1;
   uint4 kn[U], vn[U];
+  if constexpr (PF) {
 #pragma unroll
-  for (int u = 0; u < U; ++u) {
-    const int t = min(t0 + (u * NW + wave) * TPL + tl, tlast);
-    kn[u] = load_nt16(kp + (size_t)t * LPR);
-    vn[u] = load_nt16(vp + (size_t)t * LPR);
+    for (int u = 0; u < U; ++u) {
+      const int t = min(t0 + (u * NW + wave) * TPL + tl, tlast);
+      kn[u] = load16<NT>(kp + (size_t)t * LPR);
+      vn[u] = load16<NT>(vp + (size_t)t * LPR);
+    }
   }
   for (int tb = t0; tb < t1; tb += U * STEP) {
     uint4 kr[U], vr[U];
     int tok[U];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      kr[u] = kn[u];
-      vr[u] = vn[u];
       tok[u] = tb + (u * NW + wave) * TPL + tl;
+      if constexpr (PF) {
+        kr[u] = kn[u];
+        vr[u] = vn[u];
+      } else {
+        const int t = min(tok[u], tlast);
+        kr[u] = load16<NT>(kp + (size_t)t * LPR);
+        vr[u] = load16<NT>(vp + (size_t)t * LPR);
+      }
     }
-    if (tb + U * STEP < t1) {
+    if constexpr (PF) {
+      // Unconditional: past the end every row clamps to the partition's last row.
 #pragma unroll
       for (int u = 0; u < U; ++u) {
         const int t = min(tb + U * STEP + (u * NW + wave) * TPL + tl, tlast);
-        kn[u] = load_nt16(kp + (size_t)t * LPR);
-        vn[u] = load_nt16(vp + (size_t)t * LPR);
+        kn[u] = load16<NT>(kp + (size_t)t * LPR);
+        vn[u] = load16<NT>(vp + (size_t)t * LPR);
       }
     }
     // Scores in base-2 units, masked to -inf where the key is not visible.
@@ -190,20 +200,61 @@ __global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
       A = fmaf(wt, sacc[w][r][d], A);
     }
     const size_t slot = (row0 + r) * (size_t)P + p;
-    a.ws_acc[slot * D + d] = A;
-    if (d == 0) {
-      a.ws_m[slot] = (M == kNegInf) ? kNegInf : M * kLn2;  // natural-log units
-      a.ws_l[slot] = L;
+    const float mnat = (M == kNegInf) ? kNegInf : M * kLn2;  // natural-log units
+    if constexpr (FUSED) {
+      store_dev(&a.ws_acc[slot * D + d], A);  // read by another workgroup in this launch
+      if (d == 0) {
+        store_dev(&a.ws_m[slot], mnat);
+        store_dev(&a.ws_l[slot], L);
+      }
+    } else {
+      a.ws_acc[slot * D + d] = A;
+      if (d == 0) {
+        a.ws_m[slot] = mnat;
+        a.ws_l[slot] = L;
+      }
     }
+  }
+
+  if constexpr (FUSED) {
+    // The last workgroup of this (batch, kv head) to store its state combines the
+    // group's rows; every other workgroup is done.
+    __shared__ float cw[RMAX * kFusedMaxP];
+    __shared__ float cl[RMAX * kFusedMaxP];
+    __shared__ float cinv[RMAX];
+    if (!last_of_group(a.counters + (size_t)b * a.Hkv + hkv, P)) return;
+    combine_group<D, NW * 64>(a.ws_m, a.ws_l, a.ws_acc, a.o, row0, a.R, P, cw, cl, cinv);
+    if (threadIdx.x == 0) reset_counter(a.counters + (size_t)b * a.Hkv + hkv);
   }
 }
 
+// Launch shape by grid size (measured on the GQA decode and 131072-key
+// workloads): a grid that fits the chip in one round runs best with 2-wave
+// workgroups that request their next rows before using the current ones; a
+// grid several rounds deep runs best with 4-wave workgroups and no prefetch.
 template <int D, int RMAX>
 static hipError_t launch_decode_r(const DecodeParams& a, hipStream_t stream) {
-  constexpr int NW = 4;
-  constexpr int U = RMAX <= 2 ? 4 : (RMAX <= 4 ? 4 : 2);
+  constexpr int U = RMAX <= 2 ? 4 : 2;
+  const long long blocks = (long long)a.P * a.Hkv * a.B;
   dim3 grid(a.P, a.Hkv, a.B);
-  hipLaunchKernelGGL((decode_split_kernel<D, RMAX, NW, U>), grid, dim3(NW * 64), 0, stream, a);
+  const bool fused = a.counters != nullptr;
+  if (blocks <= 2048) {
+    if (fused) {
+      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 2, U, true, true, true>), grid, dim3(2 * 64),
+                         0, stream, a);
+    } else {
+      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 2, U, true>), grid, dim3(2 * 64), 0,
+                         stream, a);
+    }
+  } else {
+    if (fused) {
+      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 4, U, false, true, true>), grid,
+                         dim3(4 * 64), 0, stream, a);
+    } else {
+      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 4, U, false>), grid, dim3(4 * 64), 0,
+                         stream, a);
+    }
+  }
   return hipGetLastError();
 }
 

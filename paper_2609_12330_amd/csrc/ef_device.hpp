@@ -26,6 +26,17 @@ __device__ __forceinline__ uint4 load_nt16(const uint4* p) {
   return make_uint4(x[0], x[1], x[2], x[3]);
 }
 
+// 16-byte global load, non-temporal or regular.
+template <bool NT>
+__device__ __forceinline__ uint4 load16(const uint4* p) {
+  if constexpr (NT) {
+    return load_nt16(p);
+  } else {
+    const u32x4_t x = *reinterpret_cast<const u32x4_t*>(p);
+    return make_uint4(x[0], x[1], x[2], x[3]);
+  }
+}
+
 // bf16 (upper half of binary32) <-> fp32.
 __device__ __forceinline__ float bf16lo_to_f32(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16hi_to_f32(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }

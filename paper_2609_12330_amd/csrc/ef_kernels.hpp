@@ -21,7 +21,14 @@ struct DecodeParams {
   int P;  // partitions
   float c;  // scale * log2(e)
   int causal;
+  // Fused combine (optional): per-(batch, kv head) arrival counters, zero on entry
+  // and left zero on exit, and the output o [B][Hq][Sq][D] fp32.
+  unsigned* counters;
+  float* o;
 };
+
+// Largest partition count for which the producer combines its group itself.
+constexpr int kFusedMaxP = 64;
 
 // MFMA attention (single pass, or split producer when ws_m != nullptr).
 struct MfmaParams {

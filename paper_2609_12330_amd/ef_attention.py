@@ -194,14 +194,15 @@ def splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, partition_size=0) -> int:
 
 
 def make_workspace(q, k, partition_size=0):
-    """A uint8 tensor on q's GPU large enough for attention_splitkv on these shapes."""
+    """A zero-filled uint8 tensor on q's GPU large enough for attention_splitkv on these
+    shapes (its arrival counters must start at zero; the library leaves them zero)."""
     torch = _torch()
     if not q.is_cuda:
         raise TypeError("make_workspace needs GPU tensors (the workspace lives on q's device)")
     B, Hq, Sq, D = q.shape
     Hkv, Skv = k.shape[1], k.shape[2]
     n = splitkv_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size)
-    return torch.empty(max(n, 256), dtype=torch.uint8, device=q.device)
+    return torch.zeros(max(n, 256), dtype=torch.uint8, device=q.device)
 
 
 def workspace_views(ws, B, Hq, Sq, Skv, D, T):
@@ -214,6 +215,16 @@ def workspace_views(ws, B, Hq, Sq, Skv, D, T):
     l = f[a // 4: a // 4 + rows * P].view(rows, P)
     acc = f[2 * a // 4: 2 * a // 4 + rows * P * D].view(rows, P, D)
     return m, l, acc
+
+
+def workspace_counters(ws, B, Hq, Hkv, Sq, Skv, D, T):
+    """int32 view of the per-(batch, kv head) arrival counters of a split-KV workspace."""
+    torch = _torch()
+    rows = B * Hq * Sq
+    P = -(-Skv // T)
+    a = (rows * P * 4 + 255) // 256 * 256
+    c = (2 * a + rows * P * D * 4 + 255) // 256 * 256
+    return ws[c: c + 4 * B * Hkv].view(torch.int32)
 
 
 def attention_splitkv(q, k, v, scale: Optional[float] = None, causal: bool = False,

@@ -128,18 +128,17 @@ def test_combine_validation():
 def test_workspace_and_partition_arithmetic():
     ws = ef.ef_attention_splitkv_workspace_size
     ps = ef.ef_attention_splitkv_partition_size
-    # GQA decode, 256-key partitions: rows = 8*32, P = 16
-    rows, P, D = 256, 16, 128
-    a = (rows * P * 4 + 255) // 256 * 256
-    assert ws(8, 32, 8, 1, 4096, 128, 256) == 2 * a + rows * P * D * 4
+    def layout(rows, P, D, kv_heads):
+        a = (rows * P * 4 + 255) // 256 * 256
+        c = (2 * a + rows * P * D * 4 + 255) // 256 * 256
+        return c + kv_heads * 4
+
+    # GQA decode, 256-key partitions: rows = 8*32, P = 16, 64 kv heads
+    assert ws(8, 32, 8, 1, 4096, 128, 256) == layout(256, 16, 128, 64)
     # 131072 keys, 512 partitions of 256
-    rows, P = 32, 512
-    a = (rows * P * 4 + 255) // 256 * 256
-    assert ws(1, 32, 8, 1, 131072, 128, 256) == 2 * a + rows * P * D * 4
+    assert ws(1, 32, 8, 1, 131072, 128, 256) == layout(32, 512, 128, 8)
     # ragged: 1000 keys in partitions of 256 -> P = 4
-    rows, P = 4, 4
-    a = (rows * P * 4 + 255) // 256 * 256
-    assert ws(1, 4, 2, 1, 1000, 128, 256) == 2 * a + rows * P * 128 * 4
+    assert ws(1, 4, 2, 1, 1000, 128, 256) == layout(4, 4, 128, 2)
     assert ps(1, 4, 2, 1, 1000, 128, 256) == 256
     # the library's choice is a multiple of 64 covering Skv with B*Hkv*P near 1024 blocks
     t = ps(8, 32, 8, 1, 4096, 128, 0)

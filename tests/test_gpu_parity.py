@@ -291,7 +291,8 @@ def test_poisoned_output_fully_written_and_guard_band_intact(path):
         ef.attention_fwd(qd, kd, vd, causal=True, out=o)
     else:
         ws = ef.make_workspace(qd, kd, 64)
-        ws.fill_(255)  # NaN bit patterns everywhere
+        for t in ef.workspace_views(ws, B, Hq, Sq, Skv, D, 64):
+            t.fill_(float("nan"))  # every stored state poisoned; the counters stay zero
         ef.attention_splitkv(qd, kd, vd, causal=True, partition_size=64, workspace=ws, out=o)
     torch.cuda.synchronize()
     assert torch.isfinite(o).all()
@@ -353,3 +354,58 @@ def test_non_default_stream():
     ref = oracle.attention_ref(f64(q.cpu()), f64(k.cpu()), f64(v.cpu()), 1 / math.sqrt(128), False)
     assert_close(o, ref, "stream split")
     assert_close(o2, ref, "stream fwd")
+
+
+def test_graph_capture_replays_match_eager():
+    """Both entry points captured in a HIP graph: every replay, with eager work and
+    synchronisations between replays, equals the eager result bit for bit."""
+    announce("graph capture")
+    qd, kd, vd = (t.cuda() for t in inputs(2, 8, 2, 1, 1500, 128, seed=14))
+    qp, kp, vp = (t.cuda() for t in inputs(1, 8, 2, 200, 200, 128, seed=15))
+    ws = ef.make_workspace(qd, kd, 256)
+    e_split = ef.attention_splitkv(qd, kd, vd, partition_size=256, workspace=ws)
+    e_fwd = ef.attention_fwd(qp, kp, vp, causal=True)
+    torch.cuda.synchronize()
+    o_split = torch.empty_like(e_split)
+    o_fwd = torch.empty_like(e_fwd)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        ef.attention_splitkv(qd, kd, vd, partition_size=256, workspace=ws, out=o_split)
+        ef.attention_fwd(qp, kp, vp, causal=True, out=o_fwd)
+    other = [t.cuda() for t in inputs(1, 4, 4, 3, 300, 128, seed=16)]
+    for rep in range(3):
+        ef.attention_splitkv(*other, partition_size=64)  # eager work between replays
+        o_split.fill_(float("nan"))
+        o_fwd.fill_(float("nan"))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(o_split, e_split), f"replay {rep}: split-KV differs from eager"
+        assert torch.equal(o_fwd, e_fwd), f"replay {rep}: fwd differs from eager"
+
+
+@pytest.mark.parametrize("shape", [(8, 32, 8, 1, 4096, 128, 256), (2, 8, 2, 2, 1000, 128, 64),
+                                   (1, 32, 8, 1, 70000, 128, 2048)],
+                         ids=lambda s: "x".join(map(str, s)))
+def test_fused_combine_reuses_workspace(shape):
+    """The in-producer combine (arrival counters in the workspace): three calls in a row on
+    one workspace, each with new inputs, all match the oracle and the separate producer +
+    combine path, and the counters are back at zero after every call."""
+    B, Hq, Hkv, Sq, Skv, D, T = shape
+    announce(f"fused combine {shape}")
+    ws = None
+    for rep in range(3):
+        q, k, v = inputs(B, Hq, Hkv, Sq, Skv, D, seed=400 + rep)
+        qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+        if ws is None:
+            ws = ef.make_workspace(qd, kd, T)
+        o = ef.attention_splitkv(qd, kd, vd, causal=rep == 1, partition_size=T, workspace=ws)
+        torch.cuda.synchronize()
+        assert (ef.workspace_counters(ws, B, Hq, Hkv, Sq, Skv, D, T) == 0).all()
+        ref = oracle.attention_ref(f64(q), f64(k), f64(v), 1 / math.sqrt(D), rep == 1)
+        assert_close(o, ref, f"fused rep {rep}")
+        ws2 = ef.attention_splitkv_partials(qd, kd, vd, causal=rep == 1, partition_size=T)
+        m, l, acc = ef.workspace_views(ws2, B, Hq, Sq, Skv, D, T)
+        o2 = ef.combine(m.contiguous(), l.contiguous(), acc.contiguous())
+        torch.cuda.synchronize()
+        assert float((o.reshape(-1, D) - o2).abs().max()) <= 1e-5
