@@ -13,15 +13,23 @@
 //
 // with v_mfma_f32_32x32x16_bf16. In both products lane l owns query l % 32,
 // so the row max, the exponentials, the row sum and the rescale of the
-// carried value are lane-local; the score accumulator, converted to bf16, is
-// already in the B-operand layout of the second product. Two lanes (l and
-// l ^ 32) share a query and exchange one value per tile for the max.
+// carried value are lane-local, and the score accumulator, converted to bf16,
+// is already in the B-operand layout of the second product. Two lanes
+// (l and l ^ 32) share a query and exchange one value per tile for the max.
 //
-// K/V tiles of 64 keys go HBM -> registers -> LDS with a double buffer: the
-// loads of tile j+1 are in flight while tile j is multiplied. K is stored
-// row-major with a 16-byte-chunk XOR swizzle; V is stored transposed (V^T)
-// with its keys permuted so that each lane's 8 keys of a P^T fragment are
-// contiguous, also XOR-swizzled against bank conflicts.
+// Software pipeline over 64-key tiles: while the vector ALU turns tile j's
+// scores into weights, the matrix core already computes tile j+1's scores,
+// then tile j's values are multiplied. K is therefore staged one tile ahead
+// of V: during step j, K stage (j+1)%2 holds K of tile j+1 and V stage j%2
+// holds V of tile j, and the step writes K of tile j+2 and V of tile j+1 into
+// the two stages nobody reads during it, so one workgroup barrier per tile
+// suffices. Tiles go HBM -> registers -> LDS; each tile's buffer loads use a
+// descriptor covering exactly the workgroup's remaining key range, so rows
+// past it read as zero (no clamping or predication, and a tile after the last
+// one reads nothing). K is stored row-major and V transposed (V^T, keys
+// permuted so each lane's 8 keys of a P^T fragment are contiguous), both in
+// rows padded by 16 bytes, which keeps the fragment reads free of bank
+// conflicts while every LDS address is a per-lane base plus an immediate.
 //
 // The maximum used as the exponent reference is only moved up when a tile's
 // maximum exceeds it by more than 8 (base-2 units), so the carried sum and
@@ -38,86 +46,117 @@ namespace ef {
 
 namespace {
 
-constexpr int BN = 64;             // keys per tile
+constexpr int BN = 64;                 // keys per tile
 constexpr float kLazyThreshold = 8.f;  // base-2 headroom before the reference moves
+constexpr uint32_t kBufferFlags = 0x00020000u;  // raw 32-bit buffer access
 
 template <int D>
 struct TileGeom {
-  static constexpr int KCH = D / 8;                  // 16-byte chunks per K row
-  static constexpr int K_BYTES = BN * D * 2;         // K tile
-  static constexpr int V_BYTES = D * BN * 2;         // V^T tile
-  static constexpr int STAGE = K_BYTES + V_BYTES;
+  static constexpr int KCH = D / 8;               // 16-byte chunks per K row
+  static constexpr int K_STRIDE = 2 * D + 16;     // padded K row, bytes
+  static constexpr int V_STRIDE = 2 * BN + 16;    // padded V^T row, bytes
+  static constexpr int K_BYTES = BN * K_STRIDE;
+  static constexpr int V_BYTES = D * V_STRIDE;
+  // LDS: V^T stage 0, V^T stage 1, K stage 0, K stage 1 (all immediates < 64 KiB).
+  static constexpr int V_OFF0 = 0;
+  static constexpr int V_OFF1 = V_BYTES;
+  static constexpr int K_OFF0 = 2 * V_BYTES;
+  static constexpr int K_OFF1 = 2 * V_BYTES + K_BYTES;
+  static constexpr int LDS_BYTES = 2 * (K_BYTES + V_BYTES);
+  template <int S>
+  static constexpr int v_off() { return S == 0 ? V_OFF0 : V_OFF1; }
+  template <int S>
+  static constexpr int k_off() { return S == 0 ? K_OFF0 : K_OFF1; }
 };
-
-__device__ __forceinline__ int swz_k(int row, int kch) { return row & (kch - 1); }
-__device__ __forceinline__ int swz_v(int d) { return (d ^ (d >> 3)) & 7; }
 
 // Slot of key kappa (0..63) inside a V^T row: swap bits 2 and 3 of kappa.
 __device__ __forceinline__ int vslot(int kappa) {
   return (kappa & ~12) | ((kappa & 4) << 1) | ((kappa & 8) >> 1);
 }
 
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_over(const uint16_t* base, int rows,
+                                                              int row_bytes) {
+  const int bytes = rows > 0 ? rows * row_bytes : 0;
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), (short)0, bytes,
+                                           kBufferFlags);
+}
+
+// Cross-half exchange: max of x over lanes l and l ^ 32.
+__device__ __forceinline__ float max_with_other_half(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                  false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
 template <int D, int NW>
 struct Loader {
   using G = TileGeom<D>;
   static constexpr int NT = NW * 64;
-  static constexpr int K_CHUNKS = BN * G::KCH;          // 16-byte chunks per K tile
-  static constexpr int K_PER_T = K_CHUNKS / NT;         // per thread
-  static constexpr int V_GROUPS = (BN / 4) * G::KCH;    // (4 keys x 8 d) groups per V tile
+  static constexpr int K_CHUNKS = BN * G::KCH;        // 16-byte chunks per K tile
+  static constexpr int K_PER_T = K_CHUNKS / NT;       // per thread
+  static constexpr int V_GROUPS = (BN / 4) * G::KCH;  // (4 keys x 8 d) groups per V tile
   static constexpr int V_PER_T = (V_GROUPS + NT - 1) / NT;
   static_assert(K_CHUNKS % NT == 0, "K tile split");
   static_assert(V_GROUPS % NT == 0 || NT % V_GROUPS == 0, "V tile split");
 
   u32x4_t kreg[K_PER_T];
   u32x4_t vreg[V_PER_T][4];
+  int kvoff[K_PER_T];  // byte offset of this thread's K chunk inside the tile
+  int vvoff[V_PER_T];  // byte offset of this thread's first V row chunk inside the tile
+  int kst[K_PER_T];    // LDS byte offset of the K chunk inside a K stage
+  int vst[V_PER_T];    // LDS byte offset of the V^T group inside a V stage
+  bool vact[V_PER_T];
 
-  // Keys past the end of the range are clamped to the last valid key: the loads
-  // stay unconditional (no divergent branch, so the compiler does not have to wait
-  // for them before the compute that follows), the duplicated K rows are masked
-  // out of the scores and the duplicated V rows meet a weight of exactly 0.
-  __device__ __forceinline__ void load(const uint16_t* kh, const uint16_t* vh, int kb, int kend) {
+  __device__ __forceinline__ void init() {
     const int t = threadIdx.x;
-    const int klast = kend - 1;
 #pragma unroll
     for (int i = 0; i < K_PER_T; ++i) {
       const int id = t + i * NT;
       const int row = id / G::KCH, ch = id % G::KCH;
-      const int key = min(kb + row, klast);
-      kreg[i] = *reinterpret_cast<const u32x4_t*>(kh + (size_t)key * D + ch * 8);
+      kvoff[i] = row * (2 * D) + ch * 16;
+      kst[i] = row * G::K_STRIDE + ch * 16;
     }
 #pragma unroll
     for (int i = 0; i < V_PER_T; ++i) {
+      // 16 consecutive threads take the 16 key quads of one 8-column chunk, so each
+      // of their transposed stores fills one V^T row's 128 bytes.
       const int gid = t + i * NT;
-      const int ch = gid % G::KCH, kq = gid / G::KCH;
-      if constexpr (V_GROUPS % NT != 0) {
-        if (gid >= V_GROUPS) break;
-      }
-#pragma unroll
-      for (int x = 0; x < 4; ++x) {
-        const int key = min(kb + kq * 4 + x, klast);
-        vreg[i][x] = *reinterpret_cast<const u32x4_t*>(vh + (size_t)key * D + ch * 8);
-      }
+      vact[i] = gid < V_GROUPS;
+      const int kq = gid % 16, ch = (gid / 16) % G::KCH;
+      vvoff[i] = kq * 4 * (2 * D) + ch * 16;
+      vst[i] = ch * 8 * G::V_STRIDE + vslot(kq * 4) * 2;
     }
   }
 
-  __device__ __forceinline__ void store(char* stage) const {
-    const int t = threadIdx.x;
-    char* ks = stage;
-    char* vs = stage + G::K_BYTES;
+  // Tile loads through a descriptor covering [kb, kend) of this head's K or V.
+  __device__ __forceinline__ void load_k(const uint16_t* kh, int kb, int kend) {
+    const __amdgpu_buffer_rsrc_t rk = buffer_over(kh + (size_t)kb * D, kend - kb, 2 * D);
 #pragma unroll
-    for (int i = 0; i < K_PER_T; ++i) {
-      const int id = t + i * NT;
-      const int row = id / G::KCH, ch = id % G::KCH;
-      *reinterpret_cast<u32x4_t*>(ks + row * (2 * D) + ((ch ^ swz_k(row, G::KCH)) << 4)) = kreg[i];
-    }
+    for (int i = 0; i < K_PER_T; ++i)
+      kreg[i] = __builtin_amdgcn_raw_buffer_load_b128(rk, kvoff[i], 0, 0);
+  }
+  __device__ __forceinline__ void load_v(const uint16_t* vh, int kb, int kend) {
+    const __amdgpu_buffer_rsrc_t rv = buffer_over(vh + (size_t)kb * D, kend - kb, 2 * D);
+#pragma unroll
+    for (int i = 0; i < V_PER_T; ++i)
+#pragma unroll
+      for (int x = 0; x < 4; ++x)
+        vreg[i][x] = __builtin_amdgcn_raw_buffer_load_b128(rv, vvoff[i] + x * 2 * D, 0, 0);
+  }
+
+  template <int S>
+  __device__ __forceinline__ void store_k(char* smem) const {
+#pragma unroll
+    for (int i = 0; i < K_PER_T; ++i)
+      *reinterpret_cast<u32x4_t*>(smem + G::template k_off<S>() + kst[i]) = kreg[i];
+  }
+  template <int S>
+  __device__ __forceinline__ void store_v(char* smem) const {
 #pragma unroll
     for (int i = 0; i < V_PER_T; ++i) {
-      const int gid = t + i * NT;
-      const int ch = gid % G::KCH, kq = gid / G::KCH;
       if constexpr (V_GROUPS % NT != 0) {
-        if (gid >= V_GROUPS) break;
+        if (!vact[i]) break;
       }
-      const int slot = vslot(kq * 4);
       const u32x4_t x0 = vreg[i][0], x1 = vreg[i][1], x2 = vreg[i][2], x3 = vreg[i][3];
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
@@ -125,11 +164,10 @@ struct Loader {
         for (int half = 0; half < 2; ++half) {
           const uint32_t sel = half ? 0x07060302u : 0x05040100u;
           u32x2_t val;
-          val[0] = __builtin_amdgcn_perm(x1[w], x0[w], sel);  // keys 0,1 at d
-          val[1] = __builtin_amdgcn_perm(x3[w], x2[w], sel);  // keys 2,3 at d
-          const int d = ch * 8 + w * 2 + half;
-          const int chunk = (slot >> 3) ^ swz_v(d);
-          *reinterpret_cast<u32x2_t*>(vs + d * (2 * BN) + (chunk << 4) + ((slot & 7) << 1)) = val;
+          val[0] = __builtin_amdgcn_perm(x1[w], x0[w], sel);  // keys 0,1 at column d
+          val[1] = __builtin_amdgcn_perm(x3[w], x2[w], sel);  // keys 2,3 at column d
+          *reinterpret_cast<u32x2_t*>(smem + G::template v_off<S>() + vst[i] +
+                                      (w * 2 + half) * G::V_STRIDE) = val;
         }
       }
     }
@@ -142,12 +180,137 @@ struct Loader {
 template <int NW>
 constexpr int kWavesPerEu = NW == 4 ? 2 : 1;
 
+template <int D, bool NEG>
+struct Tile {
+  using Geo = TileGeom<D>;
+  static constexpr int KSTEPS = D / 16;  // MFMA k-steps over the head dimension
+  static constexpr int DT = D / 32;      // 32-wide output tiles along D
+
+  // S^T of the key tile in K stage S: two 32-key halves, 16-deep MFMA k-steps.
+  template <int S>
+  static __device__ __forceinline__ void scores(const char* smem, int kbase_lane,
+                                                const bf16x8_t* qf, floatx16* sacc) {
+#pragma unroll
+    for (int half = 0; half < 2; ++half)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) sacc[half][i] = 0.f;
+#pragma unroll
+    for (int s = 0; s < KSTEPS; ++s) {
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const u32x4_t kx = *reinterpret_cast<const u32x4_t*>(
+            smem + Geo::template k_off<S>() + kbase_lane + half * 32 * Geo::K_STRIDE + s * 32);
+        sacc[half] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kx),
+                                                            qf[s], sacc[half], 0, 0, 0);
+      }
+    }
+  }
+
+  // Scores in exponent-ready form (sign applied, hidden keys at -inf) and the
+  // rolling reference update; returns -reference (0 while nothing is visible).
+  static __device__ __forceinline__ float prepare(floatx16* sacc, float* x, floatx16* oacc,
+                                                  float& lsum, float& mref, float c, int kb,
+                                                  int kend, bool masked, int lim, int h) {
+#pragma unroll
+    for (int half = 0; half < 2; ++half)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) x[half * 16 + i] = NEG ? -sacc[half][i] : sacc[half][i];
+    if (masked) {
+#pragma unroll
+      for (int half = 0; half < 2; ++half)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int key = kb + half * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
+          if (key >= kend || key > lim) x[half * 16 + i] = kNegInf;
+        }
+    }
+    float tmax = fmaxf(x[0], x[1]);
+#pragma unroll
+    for (int i = 2; i < 32; ++i) tmax = fmaxf(tmax, x[i]);
+    tmax = max_with_other_half(tmax);
+    const float cand = tmax * c;  // tile maximum in base-2 units (c > 0)
+    // Move the reference only when the tile exceeds it by the threshold.
+    const bool up = cand > mref + kLazyThreshold;
+    if (__builtin_amdgcn_ballot_w64(up)) {
+      const float rs = up ? exp2_fast(mref - cand) : 1.f;  // 0 when mref = -inf
+      mref = up ? cand : mref;
+      lsum *= rs;
+#pragma unroll
+      for (int i = 0; i < DT; ++i)
+#pragma unroll
+        for (int jj = 0; jj < 16; ++jj) oacc[i][jj] *= rs;
+    }
+    return (mref == kNegInf) ? 0.f : -mref;
+  }
+
+  // Weights 2^(x*c - reference) as bf16 pairs (P^T fragments) and their row sum.
+  static __device__ __forceinline__ void weights(const float* x, float c, float mneg,
+                                                 uint32_t* pk, float& lsum) {
+    float ps0 = 0.f, ps1 = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float p0 = exp2_fast(fmaf(x[2 * i], c, mneg));
+      const float p1 = exp2_fast(fmaf(x[2 * i + 1], c, mneg));
+      ps0 += p0;
+      ps1 += p1;
+      pk[i] = pack_bf16x2(p0, p1);
+    }
+    lsum += ps0 + ps1;
+  }
+
+  // O^T += V^T * P^T over the four 16-key steps of the tile in V stage S.
+  template <int S>
+  static __device__ __forceinline__ void values(const char* smem, int vbase_lane,
+                                                const uint32_t* pk, floatx16* oacc) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      // P^T fragment: registers 8*(s%2) .. +8 of score half s/2, i.e. pk[4*s .. 4*s+3].
+      const u32x4_t pv = {pk[4 * s], pk[4 * s + 1], pk[4 * s + 2], pk[4 * s + 3]};
+      const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pv);
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const u32x4_t vx = *reinterpret_cast<const u32x4_t*>(
+            smem + Geo::template v_off<S>() + vbase_lane + dt * 32 * Geo::V_STRIDE + s * 32);
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vx), pf,
+                                                          oacc[dt], 0, 0, 0);
+      }
+    }
+  }
+};
+
+// One pipelined step on tile j (stage parity S = j % 2). On entry sacc holds
+// S^T of tile j, K stage 1-S holds tile j+1 and V stage S holds tile j. The
+// step computes tile j's weights while the matrix core computes tile j+1's
+// scores, multiplies tile j's values, and stages K of tile j+2 (into K stage
+// S, last read for tile j's scores) and V of tile j+1 (into V stage 1-S, last
+// read for tile j-1's values) before the workgroup barrier.
+template <int D, int NW, bool NEG, int S>
+__device__ __forceinline__ void pipelined_step(
+    char* smem, Loader<D, NW>& ld, const uint16_t* kh, const uint16_t* vh, int kb, int kend,
+    bool causal, int lim, int lim_lo, int h, int kbase_lane, int vbase_lane, const bf16x8_t* qf,
+    floatx16* sacc, floatx16* oacc, float& lsum, float& mref, float c) {
+  using TileT = Tile<D, NEG>;
+  ld.load_k(kh, kb + 2 * BN, kend);  // past kend the descriptors cover nothing
+  ld.load_v(vh, kb + BN, kend);
+  const bool masked = (kb + BN > kend) || (causal && kb + BN - 1 > lim_lo);
+  float x[32];
+  const float mneg = TileT::prepare(sacc, x, oacc, lsum, mref, c, kb, kend, masked, lim, h);
+  uint32_t pk[16];
+  TileT::weights(x, c, mneg, pk, lsum);
+  TileT::template scores<1 - S>(smem, kbase_lane, qf, sacc);  // tile j+1
+  TileT::template values<S>(smem, vbase_lane, pk, oacc);
+  ld.template store_k<S>(smem);
+  ld.template store_v<1 - S>(smem);
+  __syncthreads();
+}
+
 template <int D, int NW, bool NEG>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(kWavesPerEu<NW>)))
 void attn_mfma_kernel(MfmaParams a) {
   using Geo = TileGeom<D>;
-  constexpr int KSTEPS = D / 16;  // MFMA k-steps over the head dimension
-  constexpr int DT = D / 32;      // 32-wide output tiles along D
+  using TileT = Tile<D, NEG>;
+  constexpr int KSTEPS = TileT::KSTEPS;
+  constexpr int DT = TileT::DT;
   constexpr int BM = 32 * NW;
   extern __shared__ __align__(16) char smem[];
 
@@ -177,15 +340,14 @@ void attn_mfma_kernel(MfmaParams a) {
   const int lim = !rvalid ? -1 : (a.causal ? sq + off : 0x7fffffff);
 
   // Key range of this workgroup: the partition, cut at the last key any row can see.
-  int kbeg = p * a.T;
+  const int kbeg = p * a.T;
   int kend = min(kbeg + a.T, a.Skv);
-  int lim_lo = 0x7fffffff, lim_hi = 0x7fffffff;
+  int lim_lo = 0x7fffffff;
   if (a.causal) {
     const int r_lo = mt * BM;
     const int r_hi = min(mt * BM + BM, a.R) - 1;
     lim_lo = r_lo / a.G + off;
-    lim_hi = r_hi / a.G + off;
-    kend = min(kend, lim_hi + 1);
+    kend = min(kend, r_hi / a.G + off + 1);
   }
   const int ntiles = kend > kbeg ? (kend - kbeg + BN - 1) / BN : 0;
 
@@ -209,106 +371,39 @@ void attn_mfma_kernel(MfmaParams a) {
   float mref = kNegInf;  // reference maximum, base-2 units
   float lsum = 0.f;      // this lane's half of the row sum
   const float c = a.c_abs;
+  const bool causal = a.causal != 0;
+  const int kbase_lane = ql * Geo::K_STRIDE + h * 16;
+  const int vbase_lane = ql * Geo::V_STRIDE + h * 16;
 
+  // Prologue: K and V of tile 0 into stage 0, K of tile 1 into K stage 1, then
+  // tile 0's scores; the second barrier orders those K reads before stage 0 is
+  // rewritten by the first pipelined step.
   Loader<D, NW> ld;
+  ld.init();
+  floatx16 sacc[2];
   if (ntiles > 0) {
-    ld.load(kh, vh, kbeg, kend);
-    ld.store(smem);
+    ld.load_k(kh, kbeg, kend);
+    ld.load_v(vh, kbeg, kend);
+    ld.template store_k<0>(smem);
+    ld.template store_v<0>(smem);
+    ld.load_k(kh, kbeg + BN, kend);
+    ld.template store_k<1>(smem);
   }
   __syncthreads();
+  if (ntiles > 0) TileT::template scores<0>(smem, kbase_lane, qf, sacc);
+  __syncthreads();
 
-  for (int j = 0; j < ntiles; ++j) {
-    const int kb = kbeg + j * BN;
-    char* stage = smem + (j & 1) * Geo::STAGE;
-    const bool more = j + 1 < ntiles;
-    ld.load(kh, vh, kb + BN, kend);  // past the end: every key clamps to the last one
-
-    // S^T = K * Q^T for two 32-key halves of the tile.
-    floatx16 sacc[2];
-    const char* ks = stage;
-#pragma unroll
-    for (int half = 0; half < 2; ++half) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) sacc[half][i] = 0.f;
-      const int krow = half * 32 + ql;
-#pragma unroll
-      for (int s = 0; s < KSTEPS; ++s) {
-        const int ch = 2 * s + h;
-        const u32x4_t kx = *reinterpret_cast<const u32x4_t*>(
-            ks + krow * (2 * D) + ((ch ^ swz_k(krow, Geo::KCH)) << 4));
-        sacc[half] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            __builtin_bit_cast(bf16x8_t, kx), qf[s], sacc[half], 0, 0, 0);
-      }
-    }
-
-    // Mask: keys past the range or past this row's causal limit.
-    const bool need_mask = (kb + BN > kend) || (a.causal && kb + BN - 1 > lim_lo);
-    float x[32];
-#pragma unroll
-    for (int half = 0; half < 2; ++half)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) x[half * 16 + i] = NEG ? -sacc[half][i] : sacc[half][i];
-    if (need_mask) {
-#pragma unroll
-      for (int half = 0; half < 2; ++half)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = kb + half * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-          if (key >= kend || key > lim) x[half * 16 + i] = kNegInf;
-        }
-    }
-    float tmax = x[0];
-#pragma unroll
-    for (int i = 1; i < 32; ++i) tmax = fmaxf(tmax, x[i]);
-    tmax = fmaxf(tmax, shfl_xor(tmax, 32));
-    const float cand = tmax * c;  // tile maximum in base-2 units (c > 0)
-    // Move the reference only when the tile exceeds it by the threshold.
-    const bool up = cand > mref + kLazyThreshold;
-    if (__builtin_amdgcn_ballot_w64(up)) {
-      const float mnew = up ? cand : mref;
-      const float rs = up ? exp2_fast(mref - mnew) : 1.f;  // 0 when mref = -inf
-      mref = mnew;
-      lsum *= rs;
-#pragma unroll
-      for (int i = 0; i < DT; ++i)
-#pragma unroll
-        for (int jj = 0; jj < 16; ++jj) oacc[i][jj] *= rs;
-    }
-    const float mneg = (mref == kNegInf) ? 0.f : -mref;
-    float psum = 0.f;
-    uint32_t pk[16];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const float p0 = exp2_fast(fmaf(x[2 * i], c, mneg));
-      const float p1 = exp2_fast(fmaf(x[2 * i + 1], c, mneg));
-      psum += p0 + p1;
-      pk[i] = pack_bf16x2(p0, p1);
-    }
-    lsum += psum;
-
-    // O^T += V^T * P^T over the four 16-key steps of the tile.
-    const char* vs = stage + Geo::K_BYTES;
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      // P^T fragment: registers 8*(s%2) .. +8 of score half s/2, i.e. pk[4*s .. 4*s+3].
-      const u32x4_t pv = {pk[4 * s], pk[4 * s + 1], pk[4 * s + 2], pk[4 * s + 3]};
-      const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pv);
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const int d = dt * 32 + ql;
-        const int chunk = (2 * s + h) ^ swz_v(d);
-        const u32x4_t vx = *reinterpret_cast<const u32x4_t*>(vs + d * (2 * BN) + (chunk << 4));
-        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vx), pf,
-                                                          oacc[dt], 0, 0, 0);
-      }
-    }
-
-    if (more) ld.store(smem + ((j + 1) & 1) * Geo::STAGE);
-    __syncthreads();
+  for (int j = 0; j < ntiles; j += 2) {
+    const int kb0 = kbeg + j * BN;
+    pipelined_step<D, NW, NEG, 0>(smem, ld, kh, vh, kb0, kend, causal, lim, lim_lo, h,
+                                  kbase_lane, vbase_lane, qf, sacc, oacc, lsum, mref, c);
+    if (j + 1 < ntiles)
+      pipelined_step<D, NW, NEG, 1>(smem, ld, kh, vh, kb0 + BN, kend, causal, lim, lim_lo, h,
+                                    kbase_lane, vbase_lane, qf, sacc, oacc, lsum, mref, c);
   }
 
   // Row sum over both lane halves.
-  const float ltot = lsum + shfl_xor(lsum, 32);
+  const float ltot = lsum + __shfl_xor(lsum, 32, 64);
   if (!rvalid) return;
   if (a.ws_m == nullptr) {
     const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
@@ -342,16 +437,22 @@ void attn_mfma_kernel(MfmaParams a) {
   }
 }
 
+template <int D, int NW, bool NEG>
+hipError_t launch_one(const MfmaParams& a, hipStream_t stream) {
+  const size_t lds = TileGeom<D>::LDS_BYTES;
+  auto kern = attn_mfma_kernel<D, NW, NEG>;
+  // More than 64 KiB of LDS per workgroup needs the attribute; set once per kernel.
+  static const hipError_t attr = hipFuncSetAttribute(
+      reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (attr != hipSuccess) return attr;
+  dim3 grid(a.mtiles, a.P, a.B * a.Hkv);
+  hipLaunchKernelGGL(kern, grid, dim3(NW * 64), lds, stream, a);
+  return hipGetLastError();
+}
+
 template <int D, int NW>
 hipError_t launch_nw(const MfmaParams& a, bool neg, hipStream_t stream) {
-  const size_t lds = 2 * TileGeom<D>::STAGE;
-  dim3 grid(a.mtiles, a.P, a.B * a.Hkv);
-  if (neg) {
-    hipLaunchKernelGGL((attn_mfma_kernel<D, NW, true>), grid, dim3(NW * 64), lds, stream, a);
-  } else {
-    hipLaunchKernelGGL((attn_mfma_kernel<D, NW, false>), grid, dim3(NW * 64), lds, stream, a);
-  }
-  return hipGetLastError();
+  return neg ? launch_one<D, NW, true>(a, stream) : launch_one<D, NW, false>(a, stream);
 }
 
 }  // namespace
