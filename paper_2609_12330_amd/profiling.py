@@ -52,12 +52,24 @@ def kernel_stats(path):
 
 
 def counter_means(path):
-    """Mean counter value per (kernel name, counter) over dispatches."""
+    """Mean counter value per (kernel name, counter) over dispatches.
+
+    Device copies (the calibration copy) are averaged over the last three
+    dispatches only: earlier copy dispatches of the same name are the
+    benchmark's host-to-device input transfers, which the calibration copy
+    follows.
+    """
     acc = defaultdict(list)
     with open(path) as f:
-        for r in csv.DictReader(f):
-            acc[(r["Kernel_Name"], r["Counter_Name"])].append(float(r["Counter_Value"]))
-    return {k: (sum(v) / len(v), len(v)) for k, v in acc.items()}
+        rows = sorted(csv.DictReader(f), key=lambda r: int(r["Dispatch_Id"]))
+    for r in rows:
+        acc[(r["Kernel_Name"], r["Counter_Name"])].append(float(r["Counter_Value"]))
+    out = {}
+    for k, v in acc.items():
+        if any(m in k[0] for m in COPY_KERNEL_MARKERS):
+            v = v[-3:]
+        out[k] = (sum(v) / len(v), len(v))
+    return out
 
 
 def _pick(means, counter, pred):
