@@ -49,6 +49,7 @@ namespace {
 constexpr int BN = 64;                 // keys per tile
 constexpr float kLazyThreshold = 8.f;  // base-2 headroom before the reference moves
 constexpr uint32_t kBufferFlags = 0x00020000u;  // raw 32-bit buffer access
+constexpr unsigned kXcds = 8;                   // accelerator dies of the chip
 
 template <int D>
 struct TileGeom {
@@ -319,11 +320,17 @@ void attn_mfma_kernel(MfmaParams a) {
   const int h = lane >> 5;   // k-group of the MFMA operands
   const int ql = lane & 31;  // this lane's query inside the wave's 32 rows
 
-  // Workgroup -> (row tile, partition, b*Hkv). Row tiles are visited last-first so
+  // Workgroup -> (row tile, partition, b*Hkv). Workgroups are dispatched to the
+  // chip's 8 XCDs round-robin by linear id; the id is remapped so that each XCD
+  // receives a contiguous run of kv heads, and all row tiles of a head, which
+  // read the same K/V, share one XCD's L2. Row tiles are visited last-first so
   // causal tiles with the most keys start first.
-  const int mt = a.mtiles - 1 - (int)blockIdx.x;
-  const int p = blockIdx.y;
-  const int bh = blockIdx.z;
+  const unsigned nwg = gridDim.x * gridDim.y * gridDim.z;
+  unsigned lin = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  if (nwg % kXcds == 0) lin = (lin % kXcds) * (nwg / kXcds) + lin / kXcds;
+  const int mt = a.mtiles - 1 - (int)(lin % gridDim.x);
+  const int p = (int)((lin / gridDim.x) % gridDim.y);
+  const int bh = (int)(lin / (gridDim.x * gridDim.y));
   const int b = bh / a.Hkv, hkv = bh % a.Hkv;
 
   const size_t kvhead = ((size_t)b * a.Hkv + hkv) * (size_t)a.Skv * D;
