@@ -9,6 +9,7 @@ from .attention import (  # noqa: F401
     attention_ref,
     attention_splitkv_ref,
     causal_visible,
+    visible,
     combine_error_scale,
     combine_ref,
     m1_dependent_reductions,

@@ -25,7 +25,11 @@ Readings taken where the paper is silent (each listed in the design notes):
     the reducer identity (-inf, 0, 0);
   * grouped-query attention maps query head hq to kv head hq // (Hq // Hkv)
     (replication by index, section 3.1 "Replicate");
-  * partial states are kept in natural-log units (exp, not exp2).
+  * partial states are kept in natural-log units (exp, not exp2);
+  * local attention (sliding window, attention sinks; section 7.3): with a
+    causal mask, a window W > 0 keeps key j for query i only when
+    j > n_i - W (the W most recent positions, the diagonal n_i = i + Skv - Sq
+    included) or j < S for the S sink keys; windows need the causal mask.
 
 Parity status: every function here is pinned by the CPU tests (closed forms,
 invariants, a library routine and brute force); none is "parity unpinned".
@@ -65,11 +69,33 @@ def causal_visible(Sq: int, Skv: int) -> np.ndarray:
     return j <= i + (Skv - Sq)
 
 
-def _scaled_scores(qh: np.ndarray, kh: np.ndarray, scale: float, causal: bool) -> np.ndarray:
+def visible(Sq: int, Skv: int, causal: bool, window: int = 0, sinks: int = 0):
+    """Boolean [Sq, Skv] visibility, or None when every key is visible.
+
+    Causal: j <= n_i with n_i = i + Skv - Sq. With a window W > 0 (causal
+    only) key j must also satisfy j > n_i - W or j < sinks.
+    """
+    if window < 0 or sinks < 0:
+        raise ValueError("window and sinks must be >= 0")
+    if not causal:
+        if window > 0:
+            raise ValueError("a window needs the causal mask")
+        return None
+    vis = causal_visible(Sq, Skv)
+    if window > 0:
+        diag = np.arange(Sq)[:, None] + (Skv - Sq)
+        j = np.arange(Skv)[None, :]
+        vis = vis & ((j > diag - window) | (j < sinks))
+    return vis
+
+
+def _scaled_scores(qh: np.ndarray, kh: np.ndarray, scale: float, causal: bool,
+                   window: int = 0, sinks: int = 0) -> np.ndarray:
     """score = q k^T, scaled = score * scale, masked to -inf where not visible (form M0)."""
     scaled = (qh @ kh.T) * float(scale)
-    if causal:
-        scaled = np.where(causal_visible(qh.shape[0], kh.shape[0]), scaled, NEG_INF)
+    vis = visible(qh.shape[0], kh.shape[0], causal, window, sinks)
+    if vis is not None:
+        scaled = np.where(vis, scaled, NEG_INF)
     return scaled
 
 
@@ -92,11 +118,13 @@ def _softmax_rows_times_v(scaled: np.ndarray, vh: np.ndarray) -> np.ndarray:
     return out
 
 
-def attention_ref(q, k, v, scale: float, causal: bool = False) -> np.ndarray:
+def attention_ref(q, k, v, scale: float, causal: bool = False, window: int = 0,
+                  sinks: int = 0) -> np.ndarray:
     """Vanilla attention M0 (figure "attention-rewrites"), fp64, o as [B, Hq, Sq, D].
 
     The G*Sq query rows that share one kv head are evaluated per (b, hkv) so a
-    long key axis is widened one head at a time.
+    long key axis is widened one head at a time. `window` and `sinks` select
+    local attention (see `visible`).
     """
     q, k, v = _as_f64(q), _as_f64(k), _as_f64(v)
     B, Hq, Hkv, Sq, Skv, D = _check_shapes(q, k, v)
@@ -107,7 +135,7 @@ def attention_ref(q, k, v, scale: float, causal: bool = False) -> np.ndarray:
             kh, vh = k[b, hk], v[b, hk]
             for g in range(G):
                 hq = hk * G + g
-                scaled = _scaled_scores(q[b, hq], kh, scale, causal)
+                scaled = _scaled_scores(q[b, hq], kh, scale, causal, window, sinks)
                 o[b, hq] = _softmax_rows_times_v(scaled, vh)
     return o
 
@@ -148,7 +176,8 @@ def partial_state(scaled: np.ndarray, vh: np.ndarray):
     return m, l, acc
 
 
-def splitkv_partials_ref(q, k, v, scale: float, causal: bool, partition_size: int):
+def splitkv_partials_ref(q, k, v, scale: float, causal: bool, partition_size: int,
+                         window: int = 0, sinks: int = 0):
     """Stored partial states of every partition (the Collection of the rolling reduction).
 
     Returns m [rows, P], l [rows, P], acc [rows, P, D] with rows ordered as
@@ -163,14 +192,14 @@ def splitkv_partials_ref(q, k, v, scale: float, causal: bool, partition_size: in
     m = np.full((rows, P), NEG_INF)
     l = np.zeros((rows, P))
     acc = np.zeros((rows, P, D))
-    vis = causal_visible(Sq, Skv) if causal else None
+    vis = visible(Sq, Skv, causal, window, sinks)
     for b in range(B):
         for hq in range(Hq):
             hk = hq // G
             r0 = (b * Hq + hq) * Sq
             for p, (s, e) in enumerate(bounds):
                 scaled = (q[b, hq] @ k[b, hk, s:e].T) * float(scale)
-                if causal:
+                if vis is not None:
                     scaled = np.where(vis[:, s:e], scaled, NEG_INF)
                 mp, lp, ap = partial_state(scaled, v[b, hk, s:e])
                 m[r0:r0 + Sq, p] = mp
@@ -222,11 +251,12 @@ def combine_error_scale(m, l, acc) -> np.ndarray:
     return out
 
 
-def attention_splitkv_ref(q, k, v, scale: float, causal: bool, partition_size: int) -> np.ndarray:
+def attention_splitkv_ref(q, k, v, scale: float, causal: bool, partition_size: int,
+                          window: int = 0, sinks: int = 0) -> np.ndarray:
     """Split-KV attention: partial states per partition, then the combine; o as [B,Hq,Sq,D]."""
     q = _as_f64(q)
     B, Hq, Sq, D = q.shape
-    m, l, acc = splitkv_partials_ref(q, k, v, scale, causal, partition_size)
+    m, l, acc = splitkv_partials_ref(q, k, v, scale, causal, partition_size, window, sinks)
     return combine_ref(m, l, acc).reshape(B, Hq, Sq, D)
 
 
@@ -318,7 +348,7 @@ def m2_tiled_rolling(q, k, v, scale: float, causal: bool, tile: int) -> np.ndarr
 
 
 def attention_bruteforce(q: Sequence, k: Sequence, v: Sequence, scale: float,
-                         causal: bool = False) -> List:
+                         causal: bool = False, window: int = 0, sinks: int = 0) -> List:
     """Element-by-element attention with math.fsum; for shapes of a few elements only.
 
     q is nested lists [B][Hq][Sq][D]; k, v are [B][Hkv][Skv][D]; returns nested lists.
@@ -335,7 +365,10 @@ def attention_bruteforce(q: Sequence, k: Sequence, v: Sequence, scale: float,
             for i in range(Sq):
                 s = []
                 for j in range(Skv):
-                    if causal and j > i + Skv - Sq:
+                    diag = i + Skv - Sq
+                    if causal and j > diag:
+                        continue
+                    if window > 0 and j <= diag - window and j >= sinks:
                         continue
                     dot = math.fsum(float(q[b][hq][i][d]) * float(k[b][hk][j][d])
                                     for d in range(D))

@@ -493,3 +493,119 @@ def test_mutant_combine_without_weights():
     assert _fails_some_pin(mutant)
     # and the real combine over the same partials passes every pin
     assert not _fails_some_pin(lambda q, k, v, s, c: oracle.attention_splitkv_ref(q, k, v, s, c, 2))
+
+
+# ---------------------------------------------------------------------------
+# Local attention: sliding window and attention sinks (causal only).
+# ---------------------------------------------------------------------------
+
+LOCAL_SHAPES = [
+    # B, Hq, Hkv, Sq, Skv, D, window, sinks
+    (1, 2, 1, 5, 9, 8, 3, 0),
+    (1, 4, 2, 7, 20, 8, 4, 2),
+    (2, 2, 2, 1, 33, 4, 5, 3),
+    (1, 2, 1, 9, 4, 4, 2, 1),   # Sq > Skv
+    (1, 1, 1, 6, 6, 4, 100, 0),  # window wider than the key axis
+]
+
+
+def _local_visible_sets(Sq, Skv, window, sinks):
+    """Visible key index lists, written out from the definition row by row."""
+    out = []
+    for i in range(Sq):
+        n = i + Skv - Sq
+        out.append([j for j in range(Skv) if j <= n and (j > n - window or j < sinks)])
+    return out
+
+
+def test_golden_local_cases():
+    cases = json.load(open(GOLDEN))["local"]
+    consts = {"ln3": math.log(3.0)}
+
+    def val(x):
+        if isinstance(x, list):
+            return [val(y) for y in x]
+        return consts[x] if isinstance(x, str) else float(x)
+
+    for c in cases:
+        o = oracle.attention_ref(np.array(val(c["q"])), np.array(val(c["k"])),
+                                 np.array(val(c["v"])), val(c["scale"]), True, c["window"],
+                                 c["sinks"])
+        np.testing.assert_allclose(o, np.array(val(c["o"])), rtol=0, atol=1e-12)
+
+
+def test_local_uniform_logits_mean_of_visible_set():
+    for n, (B, Hq, Hkv, Sq, Skv, D, W, S) in enumerate(LOCAL_SHAPES):
+        _, k, v = _inputs(B, Hq, Hkv, Sq, Skv, D, 500 + n)
+        q = np.zeros((B, Hq, Sq, D))
+        o = oracle.attention_ref(q, k, v, 0.7, True, W, S)
+        sets = _local_visible_sets(Sq, Skv, W, S)
+        G = Hq // Hkv
+        for i, js in enumerate(sets):
+            for hq in range(Hq):
+                want = v[:, hq // G, js].mean(axis=1) if js else 0.0
+                np.testing.assert_allclose(o[:, hq, i], want, rtol=0, atol=1e-13)
+
+
+def test_local_window_one_selects_diagonal():
+    q, k, v = _inputs(1, 2, 1, 4, 10, 8, 510)
+    o = oracle.attention_ref(q * 9, k, v, 1.0, True, 1, 0)
+    for i in range(4):
+        np.testing.assert_allclose(o[0, :, i], np.repeat(v[0, :, 6 + i], 2, axis=0), rtol=0,
+                                   atol=1e-13)
+
+
+def test_local_wide_window_is_plain_causal():
+    q, k, v = _inputs(1, 4, 2, 6, 11, 8, 511)
+    np.testing.assert_allclose(oracle.attention_ref(q, k, v, 0.5, True, 11, 3),
+                               oracle.attention_ref(q, k, v, 0.5, True), rtol=0, atol=1e-15)
+
+
+def test_local_matches_sdpa_and_bruteforce():
+    for n, (B, Hq, Hkv, Sq, Skv, D, W, S) in enumerate(LOCAL_SHAPES):
+        q, k, v = _inputs(B, Hq, Hkv, Sq, Skv, D, 520 + n)
+        o = oracle.attention_ref(q, k, v, 0.4, True, W, S)
+        vis = oracle.visible(Sq, Skv, True, W, S)
+        live = vis.any(axis=1)
+        mask = torch.from_numpy(vis)
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            *(torch.from_numpy(np.ascontiguousarray(x)) for x in (q, k, v)), attn_mask=mask,
+            scale=0.4, enable_gqa=True).numpy()
+        np.testing.assert_allclose(o[:, :, live], ref[:, :, live], rtol=0, atol=1e-12)
+        if Sq * Skv * D <= 400:
+            bf = np.array(oracle.attention_bruteforce(q.tolist(), k.tolist(), v.tolist(), 0.4,
+                                                      True, W, S))
+            np.testing.assert_allclose(o, bf, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("T", [1, 3, 8])
+def test_local_split_equals_unsplit(T):
+    for n, (B, Hq, Hkv, Sq, Skv, D, W, S) in enumerate(LOCAL_SHAPES):
+        q, k, v = _inputs(B, Hq, Hkv, Sq, Skv, D, 530 + n)
+        ref = oracle.attention_ref(q, k, v, 0.6, True, W, S)
+        np.testing.assert_allclose(oracle.attention_splitkv_ref(q, k, v, 0.6, True, T, W, S),
+                                   ref, rtol=0, atol=1e-12)
+
+
+def test_local_window_needs_causal():
+    q, k, v = _inputs(1, 1, 1, 2, 4, 4, 540)
+    with pytest.raises(ValueError):
+        oracle.attention_ref(q, k, v, 1.0, False, 2, 0)
+
+
+def test_mutant_window_off_by_one(monkeypatch):
+    real = oa.visible
+
+    def bad(Sq, Skv, causal, window=0, sinks=0):
+        return real(Sq, Skv, causal, window + 1 if window else 0, sinks)
+
+    monkeypatch.setattr(oa, "visible", bad)
+    with pytest.raises(AssertionError):
+        test_golden_local_cases()
+
+
+def test_mutant_sinks_ignored(monkeypatch):
+    real = oa.visible
+    monkeypatch.setattr(oa, "visible", lambda Sq, Skv, c, w=0, s=0: real(Sq, Skv, c, w, 0))
+    with pytest.raises(AssertionError):
+        test_golden_local_cases()
