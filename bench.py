@@ -12,7 +12,9 @@ The K timed steps are captured in one HIP graph and replayed, so host launch
 cost stays out of the figure (the paper times under CUDA Graphs).
 
 Prints one JSON line. `--config` selects another workload (the causal prefill
-is reported in TFLOP/s through ef_attention_fwd).
+is reported in TFLOP/s through ef_attention_fwd; the local-attention workloads
+run through the *_local entry points and count only the keys their window and
+sinks let some query see).
 """
 
 from __future__ import annotations
@@ -40,7 +42,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
-    ap.add_argument("--config", default="gqa_decode_b8_h32x8_kv4096_d128")
+    ap.add_argument("--config", default="gqa_decode_b8_h32x8_kv4096_d128",
+                    help="workload name (see paper_2609_12330_amd/workloads.py)")
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="CPU work budget of the oracle baseline (0 disables it)")
@@ -79,14 +82,18 @@ def cpu_baseline(cfg, q, k, v, budget_s, unit_fn):
     Q, K, V = wl.to_f64(q), wl.to_f64(k), wl.to_f64(v)
     # Bound the sample: whole kv-head groups of the workload, enough for ~budget_s of work.
     B = cfg.B
-    oracle.attention_ref(Q[:1], K[:1], V[:1], cfg.scale, cfg.causal)  # warm caches and pools
+    def run():
+        oracle.attention_ref(Q[:1], K[:1], V[:1], cfg.scale, cfg.causal, window=cfg.window,
+                             sinks=cfg.sinks)
+
+    run()  # warm caches and pools
     t0 = time.perf_counter()
-    oracle.attention_ref(Q[:1], K[:1], V[:1], cfg.scale, cfg.causal)
+    run()
     one = max(time.perf_counter() - t0, 1e-6)
     reps = max(1, int(budget_s / one))
     t0 = time.perf_counter()
     for _ in range(reps):
-        oracle.attention_ref(Q[:1], K[:1], V[:1], cfg.scale, cfg.causal)
+        run()
     dt = time.perf_counter() - t0
     value = unit_fn(reps / B) / dt  # the work of `reps` batch rows of the workload per second
     return {
@@ -138,13 +145,26 @@ def main():
     stream = torch.cuda.current_stream()
     B, Hq, Hkv, Sq, Skv, D = cfg.B, cfg.Hq, cfg.Hkv, cfg.Sq, cfg.Skv, cfg.D
 
+    W, S = cfg.window, cfg.sinks
     if decode:
-        T = ef.splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, cfg.partition_size)
-        P = -(-Skv // T)
-        ws = ef.make_workspace(sets[0][0], sets[0][1], T)
+        T = ef.splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, cfg.partition_size, W, S)
+        nbytes = ef.splitkv_workspace_size(B, Hq, Hkv, Sq, Skv, D, T, W, S)
+        ws = ef.make_workspace(sets[0][0], sets[0][1], T, W, S)
+        P = ef.splitkv_partitions(Sq, Skv, T, W, S)
         wsb = ws.numel()
-        m, l, acc = ef.workspace_views(ws, B, Hq, Sq, Skv, D, T)
+        assert wsb >= nbytes
+        m, l, acc = ef.workspace_views(ws, B, Hq, Sq, Skv, D, T, W, S)
         rows = B * Hq * Sq
+
+        def whole(q, k, v, sh):
+            """The whole split-KV attention through one library call."""
+            if cfg.local:
+                return ef.ef_attention_splitkv_local(q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                                     o.data_ptr(), B, Hq, Hkv, Sq, Skv, D,
+                                                     cfg.scale, W, S, T, ws.data_ptr(), wsb, sh)
+            return ef.ef_attention_splitkv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                           B, Hq, Hkv, Sq, Skv, D, cfg.scale, cfg.causal, T,
+                                           ws.data_ptr(), wsb, sh)
 
         def produce(i):
             q, k, v = sets[i % nbuf]
@@ -156,8 +176,11 @@ def main():
                 raise RuntimeError(f"library error {st}")
 
         # The library runs the combine inside the producer when G*Sq <= 8 and P <= 64;
-        # otherwise the producer is followed by a separate combine kernel.
+        # otherwise the producer is followed by a separate combine kernel. Local
+        # workloads are timed through the whole call (there is no separate local
+        # producer entry point), so their "producer" figure includes any combine.
         fused = cfg.G * Sq <= 8 and P <= 64
+        single_call = fused or cfg.local
 
         def step(i, ev=None):
             q, k, v = sets[i % nbuf]
@@ -165,10 +188,8 @@ def main():
             sh = cur.cuda_stream
             if ev is not None:
                 ev[0].record(cur)
-            if fused:
-                st = ef.ef_attention_splitkv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
-                                             B, Hq, Hkv, Sq, Skv, D, cfg.scale, cfg.causal, T,
-                                             ws.data_ptr(), wsb, sh)
+            if single_call:
+                st = whole(q, k, v, sh)
                 if ev is not None:
                     ev[1].record(cur)
                     ev[2].record(cur)
@@ -185,8 +206,8 @@ def main():
             if st:
                 raise RuntimeError(f"library error {st}")
 
-        if fused:
-            def produce(i):  # noqa: F811  (one kernel: producer with the combine inside)
+        if single_call:
+            def produce(i):  # noqa: F811  (one call: producer with the combine inside)
                 step(i)
     else:
         T, P = Skv, 1
@@ -199,8 +220,14 @@ def main():
             cur = torch.cuda.current_stream()
             if ev is not None:
                 ev[0].record(cur)
-            st = ef.ef_attention_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B, Hq,
-                                     Hkv, Sq, Skv, D, cfg.scale, cfg.causal, cur.cuda_stream)
+            if cfg.local:
+                st = ef.ef_attention_fwd_local(q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                               o.data_ptr(), B, Hq, Hkv, Sq, Skv, D, cfg.scale, W,
+                                               S, cur.cuda_stream)
+            else:
+                st = ef.ef_attention_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                         B, Hq, Hkv, Sq, Skv, D, cfg.scale, cfg.causal,
+                                         cur.cuda_stream)
             if ev is not None:
                 ev[1].record(cur)
                 ev[2].record(cur)
@@ -272,11 +299,11 @@ def main():
     if decode:
         # Producer: algorithmic bytes = bf16 q + K + V read once (512 B per key per kv head).
         kernel = ("decode_split" if cfg.Sq * cfg.G <= 8 else "attn_mfma_split") + (
-            "_fused" if fused else "")
+            "_local" if cfg.local else "") + ("_fused" if fused else "")
         src = source_hash(*(("decode_split.hip", "group_combine.hpp") if cfg.Sq * cfg.G <= 8
                             else ("attn_mfma.hip",)), "ef_device.hpp")
-        # fused: q, K, V read and o written by the one kernel; else the producer reads q, K, V
-        alg = cfg.algorithmic_bytes() if fused else kv + q_bytes
+        # one call: q, K, V read and o written; else the producer reads q, K, V
+        alg = cfg.algorithmic_bytes() if single_call else kv + q_bytes
         achieved = alg / (prod_avg * 1e-3) / 1e9
         traffic = load_traffic(f"{kernel}_{cfg.name}", src, 1)
         roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
@@ -286,7 +313,7 @@ def main():
         unit = "GB/s"
         unit_fn = lambda batches: kv * batches / 1e9  # noqa: E731
     else:
-        kernel = "attn_mfma"
+        kernel = "attn_mfma" + ("_local" if cfg.local else "")
         src = source_hash("attn_mfma.hip", "ef_device.hpp")
         flops = cfg.flops()
         achieved = flops / (prod_avg * 1e-3) / 1e12
@@ -318,7 +345,7 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (seeded i.i.d. N(0,1) bf16 q/k/v)",
         "config": {"workload": cfg.name, "B": B, "Hq": Hq, "Hkv": Hkv, "Sq": Sq, "Skv": Skv,
-                   "D": D, "causal": bool(cfg.causal), "partition_size": T if decode else None,
+                   "D": D, "causal": bool(cfg.causal), "window": W, "sinks": S, "partition_size": T if decode else None,
                    "partitions": P, "kv_buffer_sets": nbuf, "parallelism": "single GPU"},
         "roofline": roof,
         "cpu_baseline": cpu,

@@ -35,6 +35,14 @@
  *     hipStream_t; NULL is the default stream) and the call returns without
  *     waiting; a launch failure reported by HIP returns EF_ERR_HIP.
  *   - Results are deterministic: the same inputs give bitwise equal outputs.
+ *   - Local attention (the *_local entry points; the sliding-window GQA and
+ *     attention-sink layers of section 7.3) is causal attention restricted
+ *     to a window of `window` keys plus `sinks` sink keys: with
+ *     n_i = i + (Skv - Sq), key j is visible to query i iff j <= n_i and
+ *     (j > n_i - window or j < sinks). window >= 1, sinks >= 0; a window of
+ *     Skv keys or more is plain causal attention. Keys that no query row of
+ *     a workgroup can see are not read: the kernels visit the sink keys and
+ *     the window and skip the masked middle.
  */
 #ifndef EF_ATTENTION_H
 #define EF_ATTENTION_H
@@ -57,7 +65,8 @@ typedef enum {
   EF_ERR_INVALID_PARTITION = 6,    /* partition_size is not 0 or a positive multiple of 64 */
   EF_ERR_WORKSPACE_TOO_SMALL = 7,  /* workspace is NULL or smaller than required */
   EF_ERR_INVALID_SCALE = 8,        /* scale is NaN or infinite */
-  EF_ERR_HIP = 9                   /* HIP reported an error when the work was enqueued */
+  EF_ERR_HIP = 9,                  /* HIP reported an error when the work was enqueued */
+  EF_ERR_INVALID_MASK = 10         /* local attention: window < 1 or sinks < 0 */
 } ef_status;
 
 /* Version of this ABI (EF_ABI_VERSION). */
@@ -79,6 +88,18 @@ const char* ef_status_string(int status);
 ef_status ef_attention_fwd(const void* q, const void* k, const void* v, float* o,
                            int B, int Hq, int Hkv, int Sq, int Skv, int D,
                            float scale, int causal, void* stream);
+
+/*
+ * ef_attention_fwd with local attention (causal mask, sliding window of
+ * `window` keys, `sinks` sink keys; see the conventions above). Each
+ * workgroup reads the key tiles of the sink run and of its rows' windows
+ * only; both runs feed one rolling reducer, so sink and window keys share one
+ * softmax normalisation (section 7.3, attention sinks).
+ * Returns EF_ERR_INVALID_MASK when window < 1 or sinks < 0.
+ */
+ef_status ef_attention_fwd_local(const void* q, const void* k, const void* v, float* o,
+                                 int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                 float scale, int window, int sinks, void* stream);
 
 /*
  * Partition size, in keys, that ef_attention_splitkv uses for these sizes:
@@ -139,6 +160,34 @@ ef_status ef_attention_splitkv(const void* q, const void* k, const void* v, floa
                                int B, int Hq, int Hkv, int Sq, int Skv, int D,
                                float scale, int causal, int partition_size,
                                void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Split-KV attention with local attention (causal mask, window, sinks; see
+ * the conventions above). The keys any query row of a (batch, kv head) can
+ * see lie in two runs: the sink run [0, La), La = min(round_up(sinks, 64),
+ * Skv), and the window run [Bs, Skv), Bs = max(La, round_down(max(0,
+ * Skv - Sq - window + 1), 64)). The partitions of T keys cut the
+ * concatenation of the two runs, Lv = La + Skv - Bs keys, so P = ceil(Lv / T)
+ * and no workgroup is spent on the masked middle. Workspace layout, counters
+ * and the fused-combine rule are those of ef_attention_splitkv with this P
+ * (partition p covers concatenated keys [p*T, p*T + T)).
+ * Returns EF_ERR_INVALID_MASK when window < 1 or sinks < 0.
+ */
+ef_status ef_attention_splitkv_local(const void* q, const void* k, const void* v, float* o,
+                                     int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                     float scale, int window, int sinks, int partition_size,
+                                     void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Partition size and workspace bytes of ef_attention_splitkv_local, as for
+ * the causal entry points but over the Lv keys of the two visible runs.
+ * Return 0 when the arguments are invalid (including window < 1 or sinks < 0).
+ */
+int ef_attention_splitkv_local_partition_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                              int window, int sinks, int partition_size);
+size_t ef_attention_splitkv_local_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv,
+                                                 int D, int window, int sinks,
+                                                 int partition_size);
 
 /*
  * The producer step of ef_attention_splitkv alone: the same validation and

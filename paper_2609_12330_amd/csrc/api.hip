@@ -44,17 +44,47 @@ ef_status check_io(const Shape& s, const void* q, const void* k, const void* v, 
   return EF_OK;
 }
 
-int resolve_partition(const Shape& s, int partition_size) {
+// Visible key runs of a (batch, kv head) for a causal window of `window` keys
+// and `sinks` sink keys (section 7.3). Every key of every query row lies in
+// the sink run [0, la) or the window run [bs, Skv): bs is the first key of the
+// earliest row's window (row 0, diagonal Skv - Sq) rounded down to a tile, la
+// the sink count rounded up to one. The split producers partition the
+// concatenation of the two runs (lv keys). A window of at least Skv keys hides
+// nothing beyond the causal mask and is dropped.
+ef::KeyRuns key_runs(int Sq, int Skv, int window, int sinks) {
+  ef::KeyRuns r{0, 0, Skv, 0, 0};
+  if (window <= 0 || window >= Skv) return r;
+  const int sk = sinks < Skv ? sinks : Skv;
+  int la = (sk + kTileKeys - 1) / kTileKeys * kTileKeys;
+  if (la > Skv) la = Skv;
+  long long ws = (long long)Skv - Sq - window + 1;  // window start of row 0
+  if (ws < 0) ws = 0;
+  int bs = (int)(ws / kTileKeys * kTileKeys);
+  if (bs < la) bs = la;
+  r.la = la;
+  r.bs = bs;
+  r.lv = la + (Skv - bs);
+  r.window = window;
+  r.sinks = sk;
+  return r;
+}
+
+// Keys per partition of a key axis of `keys` keys (the visible runs' length).
+int resolve_partition(const Shape& s, int keys, int partition_size) {
   if (partition_size > 0) return partition_size;
-  if (s.Skv <= 0) return kTileKeys;
+  if (keys <= 0) return kTileKeys;
   const long long kv_heads = (long long)s.B * s.Hkv;
   long long parts = (kTargetBlocks + kv_heads - 1) / kv_heads;
   if (parts < 1) parts = 1;
-  long long t = (s.Skv + parts - 1) / parts;
+  long long t = (keys + parts - 1) / parts;
   t = (t + kTileKeys - 1) / kTileKeys * kTileKeys;
   if (t < 256) t = 256;  // keep the stored state small against the K/V bytes read
-  if (t > s.Skv) t = (s.Skv + kTileKeys - 1) / kTileKeys * kTileKeys;
+  if (t > keys) t = (keys + kTileKeys - 1) / kTileKeys * kTileKeys;
   return (int)t;
+}
+
+ef_status check_mask(int window, int sinks) {
+  return (window < 1 || sinks < 0) ? EF_ERR_INVALID_MASK : EF_OK;
 }
 
 struct WsLayout {
@@ -76,7 +106,7 @@ ef_status from_hip(hipError_t e) { return e == hipSuccess ? EF_OK : EF_ERR_HIP; 
 
 ef_status launch_mfma(const Shape& s, const void* q, const void* k, const void* v, float* o,
                       float* ws_m, float* ws_l, float* ws_acc, int T, int P, float scale,
-                      int causal, hipStream_t stream) {
+                      int causal, const ef::KeyRuns& runs, hipStream_t stream) {
   ef::MfmaParams a{};
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k);
@@ -94,6 +124,7 @@ ef_status launch_mfma(const Shape& s, const void* q, const void* k, const void* 
   a.mtiles = (a.R + bm - 1) / bm;
   a.c_abs = std::fabs(scale) * ef::kLog2e;
   a.causal = causal ? 1 : 0;
+  a.runs = runs;
   return from_hip(ef::launch_mfma_attention(a, scale < 0.f, stream));
 }
 
@@ -115,41 +146,89 @@ const char* ef_status_string(int status) {
     case EF_ERR_WORKSPACE_TOO_SMALL: return "workspace is NULL or too small";
     case EF_ERR_INVALID_SCALE: return "scale is not finite";
     case EF_ERR_HIP: return "HIP error while enqueueing work";
+    case EF_ERR_INVALID_MASK: return "window must be >= 1 and sinks >= 0";
     default: return "unknown status";
   }
 }
 
-ef_status ef_attention_fwd(const void* q, const void* k, const void* v, float* o, int B, int Hq,
-                           int Hkv, int Sq, int Skv, int D, float scale, int causal,
-                           void* stream) {
-  const Shape s{B, Hq, Hkv, Sq, Skv, D};
+}  // extern "C"
+
+namespace {
+
+ef_status fwd_impl(const Shape& s, const void* q, const void* k, const void* v, float* o,
+                   float scale, int causal, const ef::KeyRuns& runs, void* stream) {
   ef_status st = check_shape(s);
   if (st != EF_OK) return st;
   st = check_io(s, q, k, v, o, scale);
   if (st != EF_OK) return st;
   if (s.rows() == 0) return EF_OK;
   hipStream_t hs = static_cast<hipStream_t>(stream);
-  if (Skv == 0) return from_hip(ef::launch_zero_fill(o, (size_t)s.rows() * D, hs));
-  return launch_mfma(s, q, k, v, o, nullptr, nullptr, nullptr, Skv, 1, scale, causal, hs);
+  if (s.Skv == 0) return from_hip(ef::launch_zero_fill(o, (size_t)s.rows() * s.D, hs));
+  return launch_mfma(s, q, k, v, o, nullptr, nullptr, nullptr, runs.lv, 1, scale, causal, runs,
+                     hs);
+}
+
+int partition_size_impl(const Shape& s, const ef::KeyRuns& runs, int partition_size) {
+  if (check_shape(s) != EF_OK) return 0;
+  if (partition_size < 0 || partition_size % kTileKeys != 0) return 0;
+  return resolve_partition(s, runs.lv, partition_size);
+}
+
+size_t workspace_size_impl(const Shape& s, const ef::KeyRuns& runs, int partition_size) {
+  if (check_shape(s) != EF_OK) return 0;
+  if (partition_size < 0 || partition_size % kTileKeys != 0) return 0;
+  if (s.rows() == 0 || s.Skv == 0) return 0;
+  const int T = resolve_partition(s, runs.lv, partition_size);
+  const long long P = (runs.lv + (long long)T - 1) / T;
+  return ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv).bytes;
+}
+
+}  // namespace
+
+extern "C" {
+
+ef_status ef_attention_fwd(const void* q, const void* k, const void* v, float* o, int B, int Hq,
+                           int Hkv, int Sq, int Skv, int D, float scale, int causal,
+                           void* stream) {
+  return fwd_impl(Shape{B, Hq, Hkv, Sq, Skv, D}, q, k, v, o, scale, causal,
+                  key_runs(Sq, Skv, 0, 0), stream);
+}
+
+ef_status ef_attention_fwd_local(const void* q, const void* k, const void* v, float* o, int B,
+                                 int Hq, int Hkv, int Sq, int Skv, int D, float scale, int window,
+                                 int sinks, void* stream) {
+  const Shape s{B, Hq, Hkv, Sq, Skv, D};
+  ef_status st = check_shape(s);
+  if (st != EF_OK) return st;
+  st = check_mask(window, sinks);
+  if (st != EF_OK) return st;
+  return fwd_impl(s, q, k, v, o, scale, 1, key_runs(Sq, Skv, window, sinks), stream);
 }
 
 int ef_attention_splitkv_partition_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
                                         int partition_size) {
-  const Shape s{B, Hq, Hkv, Sq, Skv, D};
-  if (check_shape(s) != EF_OK) return 0;
-  if (partition_size < 0 || partition_size % kTileKeys != 0) return 0;
-  return resolve_partition(s, partition_size);
+  return partition_size_impl(Shape{B, Hq, Hkv, Sq, Skv, D}, key_runs(Sq, Skv, 0, 0),
+                             partition_size);
 }
 
 size_t ef_attention_splitkv_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
                                            int partition_size) {
-  const Shape s{B, Hq, Hkv, Sq, Skv, D};
-  if (check_shape(s) != EF_OK) return 0;
-  if (partition_size < 0 || partition_size % kTileKeys != 0) return 0;
-  if (s.rows() == 0 || Skv == 0) return 0;
-  const int T = resolve_partition(s, partition_size);
-  const long long P = (Skv + (long long)T - 1) / T;
-  return ws_layout(s.rows(), P, D, (long long)B * Hkv).bytes;
+  return workspace_size_impl(Shape{B, Hq, Hkv, Sq, Skv, D}, key_runs(Sq, Skv, 0, 0),
+                             partition_size);
+}
+
+int ef_attention_splitkv_local_partition_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                              int window, int sinks, int partition_size) {
+  if (check_mask(window, sinks) != EF_OK) return 0;
+  return partition_size_impl(Shape{B, Hq, Hkv, Sq, Skv, D}, key_runs(Sq, Skv, window, sinks),
+                             partition_size);
+}
+
+size_t ef_attention_splitkv_local_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                                 int window, int sinks, int partition_size) {
+  if (check_mask(window, sinks) != EF_OK) return 0;
+  return workspace_size_impl(Shape{B, Hq, Hkv, Sq, Skv, D}, key_runs(Sq, Skv, window, sinks),
+                             partition_size);
 }
 
 }  // extern "C"
@@ -159,9 +238,10 @@ namespace {
 // Validation shared by the split-KV entry points; on success fills the
 // partition count and the workspace pointers.
 ef_status split_prepare(const Shape& s, const void* q, const void* k, const void* v,
-                        const float* o, float scale, int partition_size, void* workspace,
-                        size_t workspace_bytes, int* T_out, int* P_out, float** ws_m,
-                        float** ws_l, float** ws_acc, unsigned** counters) {
+                        const float* o, float scale, const ef::KeyRuns& runs,
+                        int partition_size, void* workspace, size_t workspace_bytes, int* T_out,
+                        int* P_out, float** ws_m, float** ws_l, float** ws_acc,
+                        unsigned** counters) {
   ef_status st = check_shape(s);
   if (st != EF_OK) return st;
   if (partition_size < 0 || partition_size % kTileKeys != 0) return EF_ERR_INVALID_PARTITION;
@@ -170,8 +250,8 @@ ef_status split_prepare(const Shape& s, const void* q, const void* k, const void
   *T_out = 0;
   *P_out = 0;
   if (s.rows() == 0 || s.Skv == 0) return EF_OK;
-  const int T = resolve_partition(s, partition_size);
-  const long long P = (s.Skv + (long long)T - 1) / T;
+  const int T = resolve_partition(s, runs.lv, partition_size);
+  const long long P = (runs.lv + (long long)T - 1) / T;
   if (P > kMaxGridYZ) return EF_ERR_INVALID_PARTITION;
   const WsLayout w = ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv);
   if (workspace == nullptr || workspace_bytes < w.bytes) return EF_ERR_WORKSPACE_TOO_SMALL;
@@ -189,8 +269,9 @@ ef_status split_prepare(const Shape& s, const void* q, const void* k, const void
 // Stores the partition states; with `counters` and `o` given (decode path only),
 // the last workgroup of each (batch, kv head) also combines them into o.
 ef_status split_produce(const Shape& s, const void* q, const void* k, const void* v, float scale,
-                        int causal, int T, int P, float* ws_m, float* ws_l, float* ws_acc,
-                        unsigned* counters, float* o, hipStream_t hs) {
+                        int causal, const ef::KeyRuns& runs, int T, int P, float* ws_m,
+                        float* ws_l, float* ws_acc, unsigned* counters, float* o,
+                        hipStream_t hs) {
   const int G = s.Hq / s.Hkv;
   const int R = G * s.Sq;
   if (R <= kDecodeMaxRows) {
@@ -210,9 +291,39 @@ ef_status split_produce(const Shape& s, const void* q, const void* k, const void
     a.causal = causal ? 1 : 0;
     a.counters = counters;
     a.o = o;
+    a.runs = runs;
     return from_hip(ef::launch_decode_split(a, hs));
   }
-  return launch_mfma(s, q, k, v, nullptr, ws_m, ws_l, ws_acc, T, P, scale, causal, hs);
+  return launch_mfma(s, q, k, v, nullptr, ws_m, ws_l, ws_acc, T, P, scale, causal, runs, hs);
+}
+
+ef_status splitkv_impl(const Shape& s, const void* q, const void* k, const void* v, float* o,
+                       float scale, int causal, const ef::KeyRuns& runs, int partition_size,
+                       void* workspace, size_t workspace_bytes, void* stream) {
+  int T = 0, P = 0;
+  float *ws_m = nullptr, *ws_l = nullptr, *ws_acc = nullptr;
+  unsigned* counters = nullptr;
+  ef_status st = split_prepare(s, q, k, v, o, scale, runs, partition_size, workspace,
+                               workspace_bytes, &T, &P, &ws_m, &ws_l, &ws_acc, &counters);
+  if (st != EF_OK || s.rows() == 0) return st;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (s.Skv == 0) return from_hip(ef::launch_zero_fill(o, (size_t)s.rows() * s.D, hs));
+  const bool fused = (s.Hq / s.Hkv) * s.Sq <= kDecodeMaxRows && P <= ef::kFusedMaxP;
+  if (fused)
+    return split_produce(s, q, k, v, scale, causal, runs, T, P, ws_m, ws_l, ws_acc, counters, o,
+                         hs);
+  st = split_produce(s, q, k, v, scale, causal, runs, T, P, ws_m, ws_l, ws_acc, nullptr, nullptr,
+                     hs);
+  if (st != EF_OK) return st;
+  ef::CombineParams c{};
+  c.m = ws_m;
+  c.l = ws_l;
+  c.acc = ws_acc;
+  c.o = o;
+  c.rows = (int)s.rows();
+  c.P = P;
+  c.D = s.D;
+  return from_hip(ef::launch_combine(c, hs));
 }
 
 }  // namespace
@@ -228,41 +339,35 @@ ef_status ef_attention_splitkv_partials(const void* q, const void* k, const void
   float *ws_m = nullptr, *ws_l = nullptr, *ws_acc = nullptr;
   unsigned* counters = nullptr;
   // The output pointer is not used here; pass q so the shared check sees a non-null pointer.
-  ef_status st = split_prepare(s, q, k, v, static_cast<const float*>(q), scale, partition_size,
-                               workspace, workspace_bytes, &T, &P, &ws_m, &ws_l, &ws_acc,
-                               &counters);
+  const ef::KeyRuns runs = key_runs(Sq, Skv, 0, 0);
+  ef_status st = split_prepare(s, q, k, v, static_cast<const float*>(q), scale, runs,
+                               partition_size, workspace, workspace_bytes, &T, &P, &ws_m, &ws_l,
+                               &ws_acc, &counters);
   if (st != EF_OK || P == 0) return st;
-  return split_produce(s, q, k, v, scale, causal, T, P, ws_m, ws_l, ws_acc, nullptr, nullptr,
-                       static_cast<hipStream_t>(stream));
+  return split_produce(s, q, k, v, scale, causal, runs, T, P, ws_m, ws_l, ws_acc, nullptr,
+                       nullptr, static_cast<hipStream_t>(stream));
 }
 
 ef_status ef_attention_splitkv(const void* q, const void* k, const void* v, float* o, int B,
                                int Hq, int Hkv, int Sq, int Skv, int D, float scale, int causal,
                                int partition_size, void* workspace, size_t workspace_bytes,
                                void* stream) {
+  return splitkv_impl(Shape{B, Hq, Hkv, Sq, Skv, D}, q, k, v, o, scale, causal,
+                      key_runs(Sq, Skv, 0, 0), partition_size, workspace, workspace_bytes,
+                      stream);
+}
+
+ef_status ef_attention_splitkv_local(const void* q, const void* k, const void* v, float* o,
+                                     int B, int Hq, int Hkv, int Sq, int Skv, int D, float scale,
+                                     int window, int sinks, int partition_size, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
   const Shape s{B, Hq, Hkv, Sq, Skv, D};
-  int T = 0, P = 0;
-  float *ws_m = nullptr, *ws_l = nullptr, *ws_acc = nullptr;
-  unsigned* counters = nullptr;
-  ef_status st = split_prepare(s, q, k, v, o, scale, partition_size, workspace, workspace_bytes,
-                               &T, &P, &ws_m, &ws_l, &ws_acc, &counters);
-  if (st != EF_OK || s.rows() == 0) return st;
-  hipStream_t hs = static_cast<hipStream_t>(stream);
-  if (Skv == 0) return from_hip(ef::launch_zero_fill(o, (size_t)s.rows() * D, hs));
-  const bool fused = (Hq / Hkv) * Sq <= kDecodeMaxRows && P <= ef::kFusedMaxP;
-  if (fused)
-    return split_produce(s, q, k, v, scale, causal, T, P, ws_m, ws_l, ws_acc, counters, o, hs);
-  st = split_produce(s, q, k, v, scale, causal, T, P, ws_m, ws_l, ws_acc, nullptr, nullptr, hs);
+  ef_status st = check_shape(s);
   if (st != EF_OK) return st;
-  ef::CombineParams c{};
-  c.m = ws_m;
-  c.l = ws_l;
-  c.acc = ws_acc;
-  c.o = o;
-  c.rows = (int)s.rows();
-  c.P = P;
-  c.D = D;
-  return from_hip(ef::launch_combine(c, hs));
+  st = check_mask(window, sinks);
+  if (st != EF_OK) return st;
+  return splitkv_impl(s, q, k, v, o, scale, 1, key_runs(Sq, Skv, window, sinks), partition_size,
+                      workspace, workspace_bytes, stream);
 }
 
 ef_status ef_attention_combine(const float* m, const float* l, const float* acc, float* o,

@@ -39,6 +39,13 @@
 //
 // In split mode the workgroup covers one key partition and stores the
 // partition's (reference, sum, value) state instead of value / sum.
+//
+// Local attention (a causal sliding window of W keys plus S sink keys; the
+// sliding-window GQA and attention-sink layers of section 7.3) visits only
+// the tiles some row of the workgroup can see: the tiles of the sink run
+// [0, S) and those from the window start of the workgroup's first row to its
+// causal end. Both runs feed the same rolling reducer, so the sink and window
+// keys share one softmax normalisation; the keys in between are never read.
 #include "ef_device.hpp"
 #include "ef_kernels.hpp"
 
@@ -88,6 +95,26 @@ __device__ __forceinline__ float max_with_other_half(float x) {
                                                   false);
   return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
+
+// Key tiles of one workgroup, in visiting order: `na` tiles of the sink run
+// starting at key a0 (keys below aend), then the tiles of the window run
+// starting at b0 (keys below bend). Without a window the sink run is empty and
+// the window run is the whole key range. Tiles past the last one cover no key.
+struct TileList {
+  int a0, aend, na, b0, bend, n;
+  int full_lo;  // a tile whose last key is at most this is below every row's causal limit
+  int win_lo;   // a tile starting at or above this key lies in every row's window
+  int sinks;    // keys below this are visible whatever the window
+  __device__ __forceinline__ int base(int j) const {
+    return j < na ? a0 + j * BN : b0 + (j - na) * BN;
+  }
+  __device__ __forceinline__ int end(int j) const { return j < na ? aend : bend; }
+  // Whether some key of tile j is hidden from some row of the workgroup.
+  __device__ __forceinline__ bool masked(int j) const {
+    const int kb = base(j);
+    return kb + BN > end(j) || kb + BN - 1 > full_lo || (kb < win_lo && kb + BN > sinks);
+  }
+};
 
 template <int D, int NW>
 struct Loader {
@@ -209,9 +236,12 @@ struct Tile {
 
   // Scores in exponent-ready form (sign applied, hidden keys at -inf) and the
   // rolling reference update; returns -reference (0 while nothing is visible).
+  // A key is hidden from this lane's row when it is past the tile's run, past
+  // the causal limit `lim`, or at most `lo` (left of the window) and not a sink.
   static __device__ __forceinline__ float prepare(floatx16* sacc, float* x, floatx16* oacc,
                                                   float& lsum, float& mref, float c, int kb,
-                                                  int kend, bool masked, int lim, int h) {
+                                                  int kend, bool masked, int lim, int lo,
+                                                  int sinks, int h) {
 #pragma unroll
     for (int half = 0; half < 2; ++half)
 #pragma unroll
@@ -222,7 +252,7 @@ struct Tile {
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int key = kb + half * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-          if (key >= kend || key > lim) x[half * 16 + i] = kNegInf;
+          if (key >= kend || key > lim || (key <= lo && key >= sinks)) x[half * 16 + i] = kNegInf;
         }
     }
     float tmax = fmaxf(x[0], x[1]);
@@ -287,15 +317,15 @@ struct Tile {
 // read for tile j-1's values) before the workgroup barrier.
 template <int D, int NW, bool NEG, int S>
 __device__ __forceinline__ void pipelined_step(
-    char* smem, Loader<D, NW>& ld, const uint16_t* kh, const uint16_t* vh, int kb, int kend,
-    bool causal, int lim, int lim_lo, int h, int kbase_lane, int vbase_lane, const bf16x8_t* qf,
+    char* smem, Loader<D, NW>& ld, const uint16_t* kh, const uint16_t* vh, const TileList& tl,
+    int j, int lim, int lo, int h, int kbase_lane, int vbase_lane, const bf16x8_t* qf,
     floatx16* sacc, floatx16* oacc, float& lsum, float& mref, float c) {
   using TileT = Tile<D, NEG>;
-  ld.load_k(kh, kb + 2 * BN, kend);  // past kend the descriptors cover nothing
-  ld.load_v(vh, kb + BN, kend);
-  const bool masked = (kb + BN > kend) || (causal && kb + BN - 1 > lim_lo);
+  ld.load_k(kh, tl.base(j + 2), tl.end(j + 2));  // past the last tile nothing is covered
+  ld.load_v(vh, tl.base(j + 1), tl.end(j + 1));
   float x[32];
-  const float mneg = TileT::prepare(sacc, x, oacc, lsum, mref, c, kb, kend, masked, lim, h);
+  const float mneg = TileT::prepare(sacc, x, oacc, lsum, mref, c, tl.base(j), tl.end(j),
+                                    tl.masked(j), lim, lo, tl.sinks, h);
   uint32_t pk[16];
   TileT::weights(x, c, mneg, pk, lsum);
   TileT::template scores<1 - S>(smem, kbase_lane, qf, sacc);  // tile j+1
@@ -345,18 +375,40 @@ void attn_mfma_kernel(MfmaParams a) {
   const size_t orow = (((size_t)b * a.Hq + (size_t)hkv * a.G + g) * a.Sq + sq);
   const int off = a.Skv - a.Sq;
   const int lim = !rvalid ? -1 : (a.causal ? sq + off : 0x7fffffff);
+  const int W = a.runs.window;
+  const int lo = W > 0 ? lim - W : INT_MIN;  // keys at or left of lo are outside the window
 
-  // Key range of this workgroup: the partition, cut at the last key any row can see.
-  const int kbeg = p * a.T;
-  int kend = min(kbeg + a.T, a.Skv);
-  int lim_lo = 0x7fffffff;
-  if (a.causal) {
-    const int r_lo = mt * BM;
-    const int r_hi = min(mt * BM + BM, a.R) - 1;
-    lim_lo = r_lo / a.G + off;
-    kend = min(kend, r_hi / a.G + off + 1);
+  // Key tiles of this workgroup. The partition is a range [v0, v1) of the
+  // virtual key axis (the sink run [0, la) followed by the window run from key
+  // bs); its part in each run is cut at the last key any row can see and, in
+  // the window run, at the first key of the earliest row's window.
+  TileList tl;
+  {
+    const int la = a.runs.la, bs = a.runs.bs;
+    const int v0 = p * a.T;
+    const int v1 = min(v0 + a.T, a.runs.lv);
+    int cend = 0x7fffffff, wbeg = 0;
+    tl.full_lo = 0x7fffffff;
+    tl.win_lo = INT_MIN;
+    if (a.causal) {
+      const int r_lo = mt * BM;
+      const int r_hi = min(mt * BM + BM, a.R) - 1;
+      tl.full_lo = r_lo / a.G + off;
+      cend = r_hi / a.G + off + 1;
+      if (W > 0) {
+        wbeg = max(0, tl.full_lo - W + 1) / BN * BN;
+        tl.win_lo = r_hi / a.G + off - W + 1;
+      }
+    }
+    tl.a0 = v0;
+    tl.aend = min(min(v1, la), cend);
+    tl.na = tl.aend > tl.a0 ? (tl.aend - tl.a0 + BN - 1) / BN : 0;
+    tl.b0 = max(bs + max(v0, la) - la, wbeg);
+    tl.bend = min(bs + v1 - la, cend);
+    tl.n = tl.na + (tl.bend > tl.b0 ? (tl.bend - tl.b0 + BN - 1) / BN : 0);
+    tl.sinks = W > 0 ? a.runs.sinks : 0;
   }
-  const int ntiles = kend > kbeg ? (kend - kbeg + BN - 1) / BN : 0;
+  const int ntiles = tl.n;
 
   // Q^T fragments (B operand): lane holds q[row][16*s + 8*h .. +8].
   bf16x8_t qf[KSTEPS];
@@ -378,7 +430,6 @@ void attn_mfma_kernel(MfmaParams a) {
   float mref = kNegInf;  // reference maximum, base-2 units
   float lsum = 0.f;      // this lane's half of the row sum
   const float c = a.c_abs;
-  const bool causal = a.causal != 0;
   const int kbase_lane = ql * Geo::K_STRIDE + h * 16;
   const int vbase_lane = ql * Geo::V_STRIDE + h * 16;
 
@@ -389,11 +440,11 @@ void attn_mfma_kernel(MfmaParams a) {
   ld.init();
   floatx16 sacc[2];
   if (ntiles > 0) {
-    ld.load_k(kh, kbeg, kend);
-    ld.load_v(vh, kbeg, kend);
+    ld.load_k(kh, tl.base(0), tl.end(0));
+    ld.load_v(vh, tl.base(0), tl.end(0));
     ld.template store_k<0>(smem);
     ld.template store_v<0>(smem);
-    ld.load_k(kh, kbeg + BN, kend);
+    ld.load_k(kh, tl.base(1), tl.end(1));
     ld.template store_k<1>(smem);
   }
   __syncthreads();
@@ -401,12 +452,11 @@ void attn_mfma_kernel(MfmaParams a) {
   __syncthreads();
 
   for (int j = 0; j < ntiles; j += 2) {
-    const int kb0 = kbeg + j * BN;
-    pipelined_step<D, NW, NEG, 0>(smem, ld, kh, vh, kb0, kend, causal, lim, lim_lo, h,
-                                  kbase_lane, vbase_lane, qf, sacc, oacc, lsum, mref, c);
+    pipelined_step<D, NW, NEG, 0>(smem, ld, kh, vh, tl, j, lim, lo, h, kbase_lane, vbase_lane,
+                                  qf, sacc, oacc, lsum, mref, c);
     if (j + 1 < ntiles)
-      pipelined_step<D, NW, NEG, 1>(smem, ld, kh, vh, kb0 + BN, kend, causal, lim, lim_lo, h,
-                                    kbase_lane, vbase_lane, qf, sacc, oacc, lsum, mref, c);
+      pipelined_step<D, NW, NEG, 1>(smem, ld, kh, vh, tl, j + 1, lim, lo, h, kbase_lane,
+                                    vbase_lane, qf, sacc, oacc, lsum, mref, c);
   }
 
   // Row sum over both lane halves.

@@ -21,7 +21,8 @@
 
 namespace ef {
 
-template <int D, int RMAX, int NW, int U, bool PF, bool NT = true, bool FUSED = false>
+template <int D, int RMAX, int NW, int U, bool PF, bool NT = true, bool FUSED = false,
+          bool LOCAL = false>
 __global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
   constexpr int LPR = D / 8;     // lanes per key row
   constexpr int TPL = 64 / LPR;  // key rows per wave-wide load
@@ -30,8 +31,12 @@ __global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
   const int tl = lane / LPR;  // row slot inside a wave-wide load
   const int dc = lane % LPR;  // which 8-element slice of D this lane holds
   const int p = blockIdx.x, hkv = blockIdx.y, b = blockIdx.z;
+  // Partition p covers virtual keys [t0, t1); with a window the virtual axis
+  // skips the keys between the sink run and the window run.
   const int t0 = p * a.T;
-  const int t1 = min(t0 + a.T, a.Skv);
+  const int t1 = min(t0 + a.T, LOCAL ? a.runs.lv : a.Skv);
+  const int la = a.runs.la, rshift = a.runs.bs - a.runs.la;
+  auto key_of = [&](int vk) { return LOCAL ? (vk < la ? vk : vk + rshift) : vk; };
   const size_t kvhead = ((size_t)b * a.Hkv + hkv) * (size_t)a.Skv;
   const uint4* kp = reinterpret_cast<const uint4*>(a.k + kvhead * D) + dc;
   const uint4* vp = reinterpret_cast<const uint4*>(a.v + kvhead * D) + dc;
@@ -71,7 +76,7 @@ __global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
   if constexpr (PF) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int t = min(t0 + (u * NW + wave) * TPL + tl, tlast);
+      const int t = key_of(min(t0 + (u * NW + wave) * TPL + tl, tlast));
       kn[u] = load16<NT>(kp + (size_t)t * LPR);
       vn[u] = load16<NT>(vp + (size_t)t * LPR);
     }
@@ -86,7 +91,7 @@ __global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
         kr[u] = kn[u];
         vr[u] = vn[u];
       } else {
-        const int t = min(tok[u], tlast);
+        const int t = key_of(min(tok[u], tlast));
         kr[u] = load16<NT>(kp + (size_t)t * LPR);
         vr[u] = load16<NT>(vp + (size_t)t * LPR);
       }
@@ -95,7 +100,7 @@ __global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
       // Unconditional: past the end every row clamps to the partition's last row.
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int t = min(tb + U * STEP + (u * NW + wave) * TPL + tl, tlast);
+        const int t = key_of(min(tb + U * STEP + (u * NW + wave) * TPL + tl, tlast));
         kn[u] = load16<NT>(kp + (size_t)t * LPR);
         vn[u] = load16<NT>(vp + (size_t)t * LPR);
       }
@@ -111,7 +116,10 @@ __global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
         d = dot2_bf16(qv[r][2], kr[u].z, d);
         d = dot2_bf16(qv[r][3], kr[u].w, d);
         d = group_sum<LPR>(d) * c;
-        s[u][r] = (tok[u] < t1 && tok[u] <= lim[r]) ? d : kNegInf;
+        const int key = key_of(tok[u]);
+        bool vis = tok[u] < t1 && key <= lim[r];
+        if constexpr (LOCAL) vis = vis && (key > lim[r] - a.runs.window || key < a.runs.sinks);
+        s[u][r] = vis ? d : kNegInf;
       }
     }
     float vf[U][8];
@@ -229,33 +237,40 @@ __global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
 }
 
 // Launch shape by grid size (measured on the GQA decode and 131072-key
-// workloads): a grid that fits the chip in one round runs best with 2-wave
+// workloads); local attention (window > 0) selects the variant that maps
+// virtual keys onto the sink and window runs: a grid that fits the chip in one round runs best with 2-wave
 // workgroups that request their next rows before using the current ones; a
 // grid several rounds deep runs best with 4-wave workgroups and no prefetch.
-template <int D, int RMAX>
-static hipError_t launch_decode_r(const DecodeParams& a, hipStream_t stream) {
+template <int D, int RMAX, bool LOCAL>
+static hipError_t launch_decode_rl(const DecodeParams& a, hipStream_t stream) {
   constexpr int U = RMAX <= 2 ? 4 : 2;
   const long long blocks = (long long)a.P * a.Hkv * a.B;
   dim3 grid(a.P, a.Hkv, a.B);
   const bool fused = a.counters != nullptr;
   if (blocks <= 2048) {
     if (fused) {
-      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 2, U, true, true, true>), grid, dim3(2 * 64),
-                         0, stream, a);
+      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 2, U, true, true, true, LOCAL>), grid,
+                         dim3(2 * 64), 0, stream, a);
     } else {
-      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 2, U, true>), grid, dim3(2 * 64), 0,
-                         stream, a);
+      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 2, U, true, true, false, LOCAL>), grid,
+                         dim3(2 * 64), 0, stream, a);
     }
   } else {
     if (fused) {
-      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 4, U, false, true, true>), grid,
+      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 4, U, false, true, true, LOCAL>), grid,
                          dim3(4 * 64), 0, stream, a);
     } else {
-      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 4, U, false>), grid, dim3(4 * 64), 0,
-                         stream, a);
+      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 4, U, false, true, false, LOCAL>), grid,
+                         dim3(4 * 64), 0, stream, a);
     }
   }
   return hipGetLastError();
+}
+
+template <int D, int RMAX>
+static hipError_t launch_decode_r(const DecodeParams& a, hipStream_t stream) {
+  return a.runs.window > 0 ? launch_decode_rl<D, RMAX, true>(a, stream)
+                           : launch_decode_rl<D, RMAX, false>(a, stream);
 }
 
 template <int D>

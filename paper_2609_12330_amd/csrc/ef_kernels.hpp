@@ -6,6 +6,16 @@
 
 namespace ef {
 
+// Visible keys of one (batch, kv head) group as a virtual key axis of length lv:
+// virtual keys [0, la) are keys [0, la) (the sink run) and virtual keys
+// [la, lv) are keys [bs, bs + lv - la) (the window run). Without a window
+// la = bs = 0 and lv = Skv. la and bs are multiples of 64, so 64-key tiles of
+// the virtual axis are 64-key tiles of the real one.
+struct KeyRuns {
+  int la, bs, lv;
+  int window, sinks;  // window > 0: key j visible to row i iff j > n_i - window or j < sinks
+};
+
 // Split-KV decode producer (VALU path, G*Sq <= 8 query rows per kv head).
 struct DecodeParams {
   const uint16_t* q;  // [B][Hq][Sq][D] bf16
@@ -25,6 +35,7 @@ struct DecodeParams {
   // and left zero on exit, and the output o [B][Hq][Sq][D] fp32.
   unsigned* counters;
   float* o;
+  KeyRuns runs;  // partitions cover the virtual key axis (T keys each)
 };
 
 // Largest partition count for which the producer combines its group itself.
@@ -45,6 +56,7 @@ struct MfmaParams {
   int mtiles;    // query-row tiles per kv head
   float c_abs;   // |scale| * log2(e)
   int causal;
+  KeyRuns runs;  // split mode: partitions cover the virtual key axis
 };
 
 // Combine of stored partial states.

@@ -29,6 +29,7 @@ STATUS_NAMES = {
     7: "EF_ERR_WORKSPACE_TOO_SMALL",
     8: "EF_ERR_INVALID_SCALE",
     9: "EF_ERR_HIP",
+    10: "EF_ERR_INVALID_MASK",
 }
 
 # Exported symbols and their C signatures (restype, argtypes).
@@ -44,6 +45,11 @@ SIGNATURES = {
     "ef_attention_splitkv_partials": (_i, [_vp, _vp, _vp, _i, _i, _i, _i, _i, _i, _f, _i, _i,
                                            _vp, _sz, _vp]),
     "ef_attention_combine": (_i, [_fp, _fp, _fp, _fp, _i, _i, _i, _vp]),
+    "ef_attention_fwd_local": (_i, [_vp, _vp, _vp, _fp, _i, _i, _i, _i, _i, _i, _f, _i, _i, _vp]),
+    "ef_attention_splitkv_local": (_i, [_vp, _vp, _vp, _fp, _i, _i, _i, _i, _i, _i, _f, _i, _i,
+                                        _i, _vp, _sz, _vp]),
+    "ef_attention_splitkv_local_partition_size": (_i, [_i, _i, _i, _i, _i, _i, _i, _i, _i]),
+    "ef_attention_splitkv_local_workspace_size": (_sz, [_i, _i, _i, _i, _i, _i, _i, _i, _i]),
 }
 
 
@@ -117,6 +123,31 @@ def ef_attention_splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, partition_size) 
     return _lib().ef_attention_splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, partition_size)
 
 
+def ef_attention_fwd_local(q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale, window, sinks,
+                           stream) -> int:
+    return _lib().ef_attention_fwd_local(q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale, window, sinks,
+                                         stream)
+
+
+def ef_attention_splitkv_local(q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale, window, sinks,
+                               partition_size, workspace, workspace_bytes, stream) -> int:
+    return _lib().ef_attention_splitkv_local(q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale, window,
+                                             sinks, partition_size, workspace, workspace_bytes,
+                                             stream)
+
+
+def ef_attention_splitkv_local_partition_size(B, Hq, Hkv, Sq, Skv, D, window, sinks,
+                                              partition_size) -> int:
+    return _lib().ef_attention_splitkv_local_partition_size(B, Hq, Hkv, Sq, Skv, D, window,
+                                                            sinks, partition_size)
+
+
+def ef_attention_splitkv_local_workspace_size(B, Hq, Hkv, Sq, Skv, D, window, sinks,
+                                              partition_size) -> int:
+    return _lib().ef_attention_splitkv_local_workspace_size(B, Hq, Hkv, Sq, Skv, D, window,
+                                                            sinks, partition_size)
+
+
 # ---------------------------------------------------------------------------
 # torch-tensor conveniences
 # ---------------------------------------------------------------------------
@@ -172,28 +203,70 @@ def _check_workspace(ws, q):
         raise ValueError("workspace must be contiguous")
 
 
+def _local(causal, window, sinks):
+    """Whether the call is local attention (window > 0), which needs the causal mask."""
+    if window < 0 or sinks < 0:
+        raise ValueError("window and sinks must be >= 0")
+    if window == 0:
+        if sinks:
+            raise ValueError("sinks need a window")
+        return False
+    if not causal:
+        raise ValueError("a window needs causal=True")
+    return True
+
+
 def attention_fwd(q, k, v, scale: Optional[float] = None, causal: bool = False, out=None,
-                  stream=None):
-    """o = softmax(scale * q k^T [masked]) v in fp32 through ef_attention_fwd."""
+                  stream=None, window: int = 0, sinks: int = 0):
+    """o = softmax(scale * q k^T [masked]) v in fp32 through ef_attention_fwd, or
+    ef_attention_fwd_local when a window is given (causal window of `window` keys plus
+    `sinks` sink keys)."""
     B, Hq, Hkv, Sq, Skv, D = _check_qkv(q, k, v)
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     o = _out(q, out)
+    if _local(causal, window, sinks):
+        st = ef_attention_fwd_local(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B, Hq,
+                                    Hkv, Sq, Skv, D, float(scale), window, sinks,
+                                    _stream_handle(stream))
+        _check(st, "ef_attention_fwd_local")
+        return o
     st = ef_attention_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B, Hq, Hkv, Sq,
                           Skv, D, float(scale), causal, _stream_handle(stream))
     _check(st, "ef_attention_fwd")
     return o
 
 
-def splitkv_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size=0) -> int:
+def splitkv_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size=0, window=0, sinks=0) -> int:
+    if window > 0:
+        return int(ef_attention_splitkv_local_workspace_size(B, Hq, Hkv, Sq, Skv, D, window, sinks,
+                                                             partition_size))
     return int(ef_attention_splitkv_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size))
 
 
-def splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, partition_size=0) -> int:
+def splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, partition_size=0, window=0, sinks=0) -> int:
+    if window > 0:
+        return int(ef_attention_splitkv_local_partition_size(B, Hq, Hkv, Sq, Skv, D, window, sinks,
+                                                             partition_size))
     return int(ef_attention_splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, partition_size))
 
 
-def make_workspace(q, k, partition_size=0):
+def local_runs(Sq, Skv, window, sinks):
+    """(La, Bs, Lv) of the header's local split-KV layout: the sink run [0, La), the
+    window run [Bs, Skv), and the Lv = La + Skv - Bs keys the partitions cut."""
+    if window <= 0 or window >= Skv:
+        return 0, 0, Skv
+    la = min(-(-min(sinks, Skv) // 64) * 64, Skv)
+    bs = max(la, max(0, Skv - Sq - window + 1) // 64 * 64)
+    return la, bs, la + Skv - bs
+
+
+def splitkv_partitions(Sq, Skv, T, window=0, sinks=0) -> int:
+    """Partition count P of a split-KV call with T keys per partition."""
+    return -(-local_runs(Sq, Skv, window, sinks)[2] // T)
+
+
+def make_workspace(q, k, partition_size=0, window=0, sinks=0):
     """A zero-filled uint8 tensor on q's GPU large enough for attention_splitkv on these
     shapes (its arrival counters must start at zero; the library leaves them zero)."""
     torch = _torch()
@@ -201,14 +274,14 @@ def make_workspace(q, k, partition_size=0):
         raise TypeError("make_workspace needs GPU tensors (the workspace lives on q's device)")
     B, Hq, Sq, D = q.shape
     Hkv, Skv = k.shape[1], k.shape[2]
-    n = splitkv_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size)
+    n = splitkv_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size, window, sinks)
     return torch.zeros(max(n, 256), dtype=torch.uint8, device=q.device)
 
 
-def workspace_views(ws, B, Hq, Sq, Skv, D, T):
+def workspace_views(ws, B, Hq, Sq, Skv, D, T, window=0, sinks=0):
     """(m [rows,P], l [rows,P], acc [rows,P,D]) fp32 views of a split-KV workspace."""
     rows = B * Hq * Sq
-    P = -(-Skv // T)
+    P = splitkv_partitions(Sq, Skv, T, window, sinks)
     a = (rows * P * 4 + 255) // 256 * 256
     f = ws.view(_torch().float32) if ws.dtype != _torch().float32 else ws
     m = f[: rows * P].view(rows, P)
@@ -217,26 +290,37 @@ def workspace_views(ws, B, Hq, Sq, Skv, D, T):
     return m, l, acc
 
 
-def workspace_counters(ws, B, Hq, Hkv, Sq, Skv, D, T):
+def workspace_counters(ws, B, Hq, Hkv, Sq, Skv, D, T, window=0, sinks=0):
     """int32 view of the per-(batch, kv head) arrival counters of a split-KV workspace."""
     torch = _torch()
     rows = B * Hq * Sq
-    P = -(-Skv // T)
+    P = splitkv_partitions(Sq, Skv, T, window, sinks)
     a = (rows * P * 4 + 255) // 256 * 256
     c = (2 * a + rows * P * D * 4 + 255) // 256 * 256
     return ws[c: c + 4 * B * Hkv].view(torch.int32)
 
 
 def attention_splitkv(q, k, v, scale: Optional[float] = None, causal: bool = False,
-                      partition_size: int = 0, workspace=None, out=None, stream=None):
-    """Split-KV attention through ef_attention_splitkv; returns o (fp32)."""
+                      partition_size: int = 0, workspace=None, out=None, stream=None,
+                      window: int = 0, sinks: int = 0):
+    """Split-KV attention through ef_attention_splitkv (ef_attention_splitkv_local when a
+    window is given); returns o (fp32)."""
     B, Hq, Hkv, Sq, Skv, D = _check_qkv(q, k, v)
     if scale is None:
         scale = 1.0 / math.sqrt(D)
     o = _out(q, out)
+    local = _local(causal, window, sinks)
     if workspace is None:
-        workspace = make_workspace(q, k, partition_size)
+        workspace = make_workspace(q, k, partition_size, window, sinks)
     _check_workspace(workspace, q)
+    if local:
+        st = ef_attention_splitkv_local(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B,
+                                        Hq, Hkv, Sq, Skv, D, float(scale), window, sinks,
+                                        partition_size, workspace.data_ptr(),
+                                        workspace.numel() * workspace.element_size(),
+                                        _stream_handle(stream))
+        _check(st, "ef_attention_splitkv_local")
+        return o
     st = ef_attention_splitkv(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B, Hq, Hkv,
                               Sq, Skv, D, float(scale), causal, partition_size,
                               workspace.data_ptr(), workspace.numel() * workspace.element_size(),

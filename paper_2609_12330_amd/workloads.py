@@ -10,7 +10,9 @@ the caller's seed: q, then k, then v, each as float32 ``randn`` of shape
 The paper's workloads are causal multi-head attention in decode and prefill
 over Llama 2 / BERT style shapes (section 7.1, "Workloads"); its benchmark
 suites are not available, so these i.i.d. N(0, 1) tensors of the same layout
-stand in for them.
+stand in for them. The local-attention workloads follow the sliding-window GQA
+(1, 4096, 16K) and attention-sink (1, 1024, 32K) layers of section 7.3, read
+as (batch, query tokens, key tokens) with a 4096-key window and 4 sink keys.
 """
 
 from __future__ import annotations
@@ -37,6 +39,12 @@ class AttentionConfig:
     partition_size: int = 0  # split-KV partition (tokens); 0 = unsplit / heuristic
     q_mult: float = 1.0  # q = bf16(q_mult * N(0,1)); 2.0 sharpens the softmax
     scale: float = dataclasses.field(default=float("nan"))
+    window: int = 0  # local attention: keys j > n_i - window are visible (causal only)
+    sinks: int = 0   # ... and keys j < sinks
+
+    @property
+    def local(self) -> bool:
+        return self.window > 0
 
     def __post_init__(self):
         if math.isnan(self.scale):
@@ -46,21 +54,44 @@ class AttentionConfig:
     def G(self) -> int:
         return self.Hq // self.Hkv
 
+    def _row_keys(self, n: int) -> int:
+        """Keys visible to a query row whose causal diagonal is key n."""
+        if n < 0:
+            return 0
+        top = min(self.Skv, n + 1)
+        if not self.local:
+            return top
+        lo = max(0, n - self.window + 1)
+        return (top - lo) + min(self.sinks, lo)
+
     def visible_pairs(self) -> int:
         """Number of (query, key) pairs the mask leaves visible, over the batch and heads."""
         if not self.causal:
             per_head = self.Sq * self.Skv
         else:
             off = self.Skv - self.Sq
-            per_head = sum(max(0, min(self.Skv, i + off + 1)) for i in range(self.Sq))
+            per_head = sum(self._row_keys(i + off) for i in range(self.Sq))
         return self.B * self.Hq * per_head
+
+    def visible_keys(self) -> int:
+        """Keys of one kv head that at least one query row can see."""
+        if not self.causal:
+            return self.Skv
+        n_lo, n_hi = self.Skv - self.Sq, self.Skv - 1
+        if n_hi < 0:
+            return 0
+        if not self.local:
+            return n_hi + 1
+        lo = max(0, n_lo - self.window + 1)
+        return (n_hi + 1 - lo) + min(self.sinks, lo)
 
     def flops(self) -> int:
         """Algorithmic flops: 2*D for q.k plus 2*D for p*v per visible pair."""
         return 4 * self.D * self.visible_pairs()
 
     def kv_bytes(self) -> int:
-        return 2 * self.B * self.Hkv * self.Skv * self.D * 2
+        """K and V bytes of every key some query row can see, read once."""
+        return 2 * self.B * self.Hkv * self.visible_keys() * self.D * 2
 
     def algorithmic_bytes(self) -> int:
         """bf16 q, k, v read once plus the fp32 output written once."""
@@ -84,10 +115,28 @@ CONFIGS: Tuple[AttentionConfig, ...] = (
                     causal=True),
 )
 
-CONFIG_BY_NAME: Dict[str, AttentionConfig] = {c.name: c for c in CONFIGS}
+# Local attention (section 7.3): the sliding-window GQA layer (Mistral-style
+# 32 query / 8 kv heads, 4096-key window) over 4096 new tokens of a 16K
+# context, the attention-sink layer (Llama-2-style 32-head MHA, 4 sinks and a
+# 4096-key window) over 1024 new tokens of a 32K context, and one-token decode
+# steps of both over 8 sequences.
+LOCAL_CONFIGS: Tuple[AttentionConfig, ...] = (
+    AttentionConfig("swa_prefill_b1_h32x8_q4096_kv16384_w4096_d128", 1, 32, 8, 4096, 16384, 128,
+                    causal=True, window=4096),
+    AttentionConfig("sink_chunk_b1_h32_q1024_kv32768_w4096_s4_d128", 1, 32, 32, 1024, 32768, 128,
+                    causal=True, window=4096, sinks=4),
+    AttentionConfig("swa_decode_b8_h32x8_kv16384_w4096_d128", 8, 32, 8, 1, 16384, 128,
+                    causal=True, window=4096),
+    AttentionConfig("sink_decode_b8_h32_kv32768_w4096_s4_d128", 8, 32, 32, 1, 32768, 128,
+                    causal=True, window=4096, sinks=4),
+)
 
-# Default seed of each workload: its position in CONFIGS, counted from 1.
-DEFAULT_SEED: Dict[str, int] = {c.name: i + 1 for i, c in enumerate(CONFIGS)}
+ALL_CONFIGS: Tuple[AttentionConfig, ...] = CONFIGS + LOCAL_CONFIGS
+
+CONFIG_BY_NAME: Dict[str, AttentionConfig] = {c.name: c for c in ALL_CONFIGS}
+
+# Default seed of each workload: its position in ALL_CONFIGS, counted from 1.
+DEFAULT_SEED: Dict[str, int] = {c.name: i + 1 for i, c in enumerate(ALL_CONFIGS)}
 
 
 def make_inputs(cfg: AttentionConfig, seed: int):

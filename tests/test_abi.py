@@ -35,7 +35,9 @@ def test_header_declares_the_entry_points():
     names = header_functions()
     for n in ("ef_attention_fwd", "ef_attention_splitkv", "ef_attention_combine",
               "ef_attention_splitkv_workspace_size", "ef_attention_splitkv_partition_size",
-              "ef_status_string", "ef_abi_version"):
+              "ef_attention_fwd_local", "ef_attention_splitkv_local",
+              "ef_attention_splitkv_local_workspace_size",
+              "ef_attention_splitkv_local_partition_size", "ef_status_string", "ef_abi_version"):
         assert n in names
     assert set(names) == set(ef.SIGNATURES), "binding signatures must cover the header exactly"
 
@@ -51,8 +53,9 @@ def test_library_exports_every_header_symbol():
 @needs_lib
 def test_status_strings():
     lib = ef.library()
-    for s in range(0, 10):
+    for s in range(0, 11):
         assert lib.ef_status_string(s)
+        assert lib.ef_status_string(s) != b"unknown status"
     assert lib.ef_status_string(0) == b"ok"
     assert lib.ef_status_string(1234) == b"unknown status"
 
@@ -74,8 +77,27 @@ def split(**kw):
                                    a["ws"], a["wsb"], a["stream"])
 
 
+def fwd_local(window=64, sinks=4, **kw):
+    a = dict(q=A, k=A, v=A, o=A, B=1, Hq=4, Hkv=2, Sq=8, Skv=16, D=128, scale=0.1, causal=1,
+             stream=None)
+    a.update(kw)
+    return ef.ef_attention_fwd_local(a["q"], a["k"], a["v"], a["o"], a["B"], a["Hq"], a["Hkv"],
+                                     a["Sq"], a["Skv"], a["D"], a["scale"], window, sinks,
+                                     a["stream"])
+
+
+def split_local(window=64, sinks=4, **kw):
+    a = dict(q=A, k=A, v=A, o=A, B=1, Hq=4, Hkv=2, Sq=1, Skv=1000, D=128, scale=0.1, causal=1,
+             T=256, ws=A, wsb=1 << 30, stream=None)
+    a.update(kw)
+    return ef.ef_attention_splitkv_local(a["q"], a["k"], a["v"], a["o"], a["B"], a["Hq"],
+                                         a["Hkv"], a["Sq"], a["Skv"], a["D"], a["scale"], window,
+                                         sinks, a["T"], a["ws"], a["wsb"], a["stream"])
+
+
 @needs_lib
-@pytest.mark.parametrize("call", [fwd, split], ids=["fwd", "splitkv"])
+@pytest.mark.parametrize("call", [fwd, split, fwd_local, split_local],
+                         ids=["fwd", "splitkv", "fwd_local", "splitkv_local"])
 def test_validation_errors(call):
     assert call(D=96) == 4
     assert call(D=0) == 4
@@ -100,6 +122,27 @@ def test_validation_errors(call):
     assert call(B=0) == 0
     assert call(Sq=0) == 0
     assert call(B=0, q=None, o=None) == 0
+
+
+@needs_lib
+@pytest.mark.parametrize("call", [fwd_local, split_local], ids=["fwd_local", "splitkv_local"])
+def test_local_mask_validation(call):
+    assert call(window=0) == 10
+    assert call(window=-5) == 10
+    assert call(sinks=-1) == 10
+    assert call(window=0, B=0) == 10  # the mask is checked even when nothing is computed
+    assert call(window=0, D=96) == 4  # shape errors come first
+    assert call(window=1, sinks=0, B=0) == 0
+
+
+@needs_lib
+def test_splitkv_local_specific_validation():
+    need = ef.ef_attention_splitkv_local_workspace_size(1, 4, 2, 1, 1000, 128, 64, 4, 256)
+    assert need > 0
+    assert split_local(wsb=need - 1) == 7
+    assert split_local(ws=None) == 7
+    assert split_local(T=100) == 6
+    assert split_local(ws=MIS, wsb=need) == 5
 
 
 @needs_lib
@@ -150,6 +193,51 @@ def test_workspace_and_partition_arithmetic():
     assert ws(1, 4, 2, 1, 1000, 128, 100) == 0
     assert ws(0, 4, 2, 1, 1000, 128, 256) == 0
     assert ws(1, 4, 2, 1, 0, 128, 256) == 0
+
+
+def _layout(rows, P, D, kv_heads):
+    a = (rows * P * 4 + 255) // 256 * 256
+    c = (2 * a + rows * P * D * 4 + 255) // 256 * 256
+    return c + kv_heads * 4
+
+
+def _runs(Sq, Skv, W, S):
+    """Visible key runs as the header documents them: (La, Bs, Lv)."""
+    if W >= Skv:
+        return 0, 0, Skv
+    la = min(-(-min(S, Skv) // 64) * 64, Skv)
+    bs = max(la, max(0, Skv - Sq - W + 1) // 64 * 64)
+    return la, bs, la + Skv - bs
+
+
+@needs_lib
+def test_local_workspace_and_partition_arithmetic():
+    ws = ef.ef_attention_splitkv_local_workspace_size
+    ps = ef.ef_attention_splitkv_local_partition_size
+    # sliding-window decode: 16384 keys, window 4096 -> the window run is the last 4096 keys
+    assert _runs(1, 16384, 4096, 0) == (0, 12288, 4096)
+    assert ws(8, 32, 8, 1, 16384, 128, 4096, 0, 256) == _layout(256, 16, 128, 64)
+    # with 4 sinks the sink run adds one 64-key tile: 4160 keys, 17 partitions of 256
+    assert _runs(1, 32768, 4096, 4) == (64, 28672, 4160)
+    assert ws(8, 32, 32, 1, 32768, 128, 4096, 4, 256) == _layout(256, 17, 128, 256)
+    # ragged: window start 1000 - 3 - 100 + 1 = 898 -> 896; 64 + 104 = 168 keys
+    assert _runs(3, 1000, 100, 10) == (64, 896, 168)
+    assert ws(1, 4, 2, 3, 1000, 128, 100, 10, 64) == _layout(12, 3, 128, 2)
+    # prefill: row 0's window starts at key 0, so nothing is skipped at the head level
+    assert ws(1, 4, 2, 500, 500, 128, 100, 4, 64) == _layout(2000, 8, 128, 2)
+    # a window of Skv keys or more is plain causal attention
+    assert ws(2, 8, 2, 1, 1000, 128, 1000, 7, 0) == ef.ef_attention_splitkv_workspace_size(
+        2, 8, 2, 1, 1000, 128, 0)
+    assert ps(2, 8, 2, 1, 1000, 128, 5000, 0, 0) == ef.ef_attention_splitkv_partition_size(
+        2, 8, 2, 1, 1000, 128, 0)
+    # the library's partition choice splits the visible runs (4160 keys), not the whole
+    # key axis: 128 partitions per kv head would be wanted, the 256-key floor gives 17
+    assert ps(1, 32, 8, 1, 131072, 128, 4096, 4, 0) == 256
+    assert ps(1, 32, 8, 1, 131072, 128, 131072, 4, 0) == 1024 == ef.ef_attention_splitkv_partition_size(
+        1, 32, 8, 1, 131072, 128, 0)
+    assert ps(1, 4, 2, 1, 1000, 128, 0, 0, 0) == 0
+    assert ws(1, 4, 2, 1, 1000, 128, 64, -1, 0) == 0
+    assert ps(1, 4, 2, 1, 1000, 128, 64, 0, 100) == 0
 
 
 def test_binding_fails_loudly_without_library(monkeypatch):

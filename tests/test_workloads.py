@@ -49,3 +49,42 @@ def test_partials_generator_empty_slots():
     empty = torch.isneginf(m)
     assert empty.any() and (~empty).any()
     assert (l[empty] == 0).all() and (acc[empty] == 0).all()
+
+
+def _brute_visible(Sq, Skv, window, sinks):
+    """Visible (query, key) pairs written out with loops."""
+    vis = []
+    for i in range(Sq):
+        n = i + Skv - Sq
+        row = []
+        for j in range(Skv):
+            ok = j <= n and (window == 0 or j > n - window or j < sinks)
+            row.append(ok)
+        vis.append(row)
+    return vis
+
+
+def test_local_accounting_matches_brute_force():
+    for Sq, Skv, W, S in [(1, 300, 64, 0), (5, 300, 64, 3), (70, 200, 16, 20), (10, 8, 3, 1),
+                          (40, 40, 100, 2), (3, 500, 1, 0)]:
+        cfg = wl.AttentionConfig("t", 2, 4, 2, Sq, Skv, 64, causal=True, window=W, sinks=S)
+        vis = _brute_visible(Sq, Skv, W, S)
+        pairs = sum(sum(r) for r in vis)
+        keys = sum(any(vis[i][j] for i in range(Sq)) for j in range(Skv))
+        assert cfg.visible_pairs() == 2 * 4 * pairs, (Sq, Skv, W, S)
+        assert cfg.visible_keys() == keys, (Sq, Skv, W, S)
+        assert cfg.kv_bytes() == 2 * 2 * 2 * keys * 64 * 2
+
+
+def test_local_workloads():
+    c = wl.CONFIG_BY_NAME
+    swa = c["swa_decode_b8_h32x8_kv16384_w4096_d128"]
+    assert swa.visible_keys() == 4096 and swa.kv_bytes() == 2 * 8 * 8 * 4096 * 128 * 2
+    snk = c["sink_decode_b8_h32_kv32768_w4096_s4_d128"]
+    assert snk.visible_keys() == 4100
+    pre = c["swa_prefill_b1_h32x8_q4096_kv16384_w4096_d128"]
+    assert pre.visible_pairs() == 32 * 4096 * 4096
+    chunk = c["sink_chunk_b1_h32_q1024_kv32768_w4096_s4_d128"]
+    assert chunk.visible_pairs() == 32 * 1024 * (4096 + 4)
+    assert chunk.visible_keys() == 4096 + 1023 + 4
+    assert len(set(wl.DEFAULT_SEED.values())) == len(wl.ALL_CONFIGS)
