@@ -117,14 +117,15 @@ int ef_attention_splitkv_partition_size(int B, int Hq, int Hkv, int Sq, int Skv,
  *     m   [rows][P]    fp32 at byte 0
  *     l   [rows][P]    fp32 at byte  A = round_up(rows*P*4, 256)
  *     acc [rows][P][D] fp32 at byte 2*A
- *     counters [B*Hkv] uint32 at byte C = round_up(2*A + rows*P*D*4, 256)
+ *     counters [B*Hkv][64] uint32 at byte C = round_up(2*A + rows*P*D*4, 256)
  * with row = (b*Hq + hq)*Sq + sq: a reference point m for the scaled scores
  * s of the row's visible keys in partition p (natural-log units; at most the
  * partition maximum and within 8*ln(2) of it), l = sum exp(s - m) and
  * acc = sum exp(s - m) * v. (m, l, acc) and (m', l*e^(m-m'), acc*e^(m-m'))
  * describe the same state. A partition with no visible key holds the reducer
  * identity (-inf, 0, 0). The counters are arrival counters of the fused
- * combine (see ef_attention_splitkv).
+ * combine (see ef_attention_splitkv): word 0 of each 256-byte slot
+ * counters[b*Hkv + hk] serves one (batch, kv head); the rest is padding.
  */
 size_t ef_attention_splitkv_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
                                            int partition_size);

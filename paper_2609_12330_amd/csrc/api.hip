@@ -98,7 +98,7 @@ WsLayout ws_layout(long long rows, long long P, int D, long long kv_heads) {
   w.l_off = a;
   w.acc_off = 2 * a;
   w.cnt_off = ef::ws_align256(2 * a + (size_t)(rows * P) * (size_t)D * sizeof(float));
-  w.bytes = w.cnt_off + (size_t)kv_heads * sizeof(unsigned);
+  w.bytes = w.cnt_off + (size_t)kv_heads * ef::kCounterStride * sizeof(unsigned);
   return w;
 }
 

@@ -82,9 +82,11 @@ __device__ __forceinline__ int vslot(int kappa) {
   return (kappa & ~12) | ((kappa & 4) << 1) | ((kappa & 8) >> 1);
 }
 
+// Descriptor over the rows [0, rows) of a tile starting at `base`; only the
+// tile's own BN rows are ever read through it, so it covers at most those.
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_over(const uint16_t* base, int rows,
                                                               int row_bytes) {
-  const int bytes = rows > 0 ? rows * row_bytes : 0;
+  const int bytes = rows > 0 ? min(rows, BN) * row_bytes : 0;
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), (short)0, bytes,
                                            kBufferFlags);
 }

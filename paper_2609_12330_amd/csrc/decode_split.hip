@@ -8,29 +8,63 @@
 // registers, and the reduced state of the partition is stored for a later
 // combine (section 3.3 "Collection"; section 4.4 storage rule).
 //
-// Lane layout: a key row of D bf16 is read by D/8 adjacent lanes, 16 bytes
-// each, so one wave-wide load covers 64*16 contiguous bytes (4 rows at
-// D = 128). Every lane keeps its 8-element slice of each query row; q.k is a
-// packed-bf16 dot product followed by a DPP sum over the row's lanes, so all
-// lanes of a row group end up with the full score. Each row group carries its
-// own rolling state; the groups of a wave and the waves of the workgroup are
-// merged with the same reducer at the end.
+// Lane layout: a key row of D bf16 is spread over LPR = D / (8 CH) adjacent
+// lanes, each holding CH 16-byte chunks of it (chunks dc, dc + LPR, ...), so
+// the CH loads of a wave read 64/LPR whole rows, each load whole 128-byte
+// lines when LPR = 8. Every lane keeps the same chunks of each query row; q.k
+// is a packed-bf16 dot product over the lane's chunks followed by a DPP sum
+// over the row's lanes, so all lanes of a row group end up with the score.
+//
+// Loads go through buffer descriptors over the partition's rows (rows past
+// it read as zero), two register sets deep. The arithmetic per key is kept
+// small, since with a handful of waves per SIMD it does not hide entirely
+// behind the loads:
+//  - a negative scale is moved into q (bf16 negation is exact), so the
+//    scale c is positive and the running maximum can be taken on raw q.k;
+//  - the exponent reference moves only when a key exceeds it by more than
+//    8 in base-2 units (the carried sum and value are rescaled then, which
+//    keeps every weight below 2^8 and is exact for any reference point);
+//  - p.V runs as packed-bf16 dot products over pairs of keys (one
+//    instruction per value element and pair), with the weights rounded to
+//    bf16 as the matrix-core kernel does; the sum l uses the fp32 weights.
+// Each row group carries its own rolling state; the groups of a wave and the
+// waves of the workgroup are merged with the same reducer at the end.
 #include "ef_device.hpp"
 #include "ef_kernels.hpp"
 #include "group_combine.hpp"
 
 namespace ef {
 
-template <int D, int RMAX, int NW, int U, bool PF, bool NT = true, bool FUSED = false,
-          bool LOCAL = false>
-__global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
-  constexpr int LPR = D / 8;     // lanes per key row
-  constexpr int TPL = 64 / LPR;  // key rows per wave-wide load
+namespace {
+
+constexpr float kMoveThreshold = 8.f;  // base-2 headroom before the reference moves
+constexpr uint32_t kBufferFlags = 0x00020000u;  // raw 32-bit buffer access
+constexpr int kNonTemporal = 2;                 // cache policy of streamed loads
+
+// Pairs (x of key a, x of key b) of the bf16 elements 2w (lo) and 2w+1 (hi) of
+// two packed words, for a packed-bf16 dot product over the two keys.
+__device__ __forceinline__ uint32_t pair_lo(uint32_t a, uint32_t b) {
+  return __builtin_amdgcn_perm(b, a, 0x05040100u);
+}
+__device__ __forceinline__ uint32_t pair_hi(uint32_t a, uint32_t b) {
+  return __builtin_amdgcn_perm(b, a, 0x07060302u);
+}
+
+}  // namespace
+
+// One partition p of the keys of kv head hkv of batch b, by the NW waves of the
+// calling workgroup.
+template <int D, int RMAX, int NW, int U, int CH, bool FUSED, bool LOCAL>
+__device__ __forceinline__ void decode_partition(const DecodeParams& a, const int p, const int hkv,
+                                                 const int b) {
+  constexpr int LPR = D / (8 * CH);  // lanes per key row
+  constexpr int TPL = 64 / LPR;      // key rows per wave-wide load
+  constexpr int DL = 8 * CH;         // value elements per lane and row
+  static_assert(U % 2 == 0, "keys are paired across the U slots");
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int tl = lane / LPR;  // row slot inside a wave-wide load
-  const int dc = lane % LPR;  // which 8-element slice of D this lane holds
-  const int p = blockIdx.x, hkv = blockIdx.y, b = blockIdx.z;
+  const int dc = lane % LPR;  // first 16-byte chunk of the row this lane holds
   // Partition p covers virtual keys [t0, t1); with a window the virtual axis
   // skips the keys between the sink run and the window run.
   const int t0 = p * a.T;
@@ -38,145 +72,202 @@ __global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
   const int la = a.runs.la, rshift = a.runs.bs - a.runs.la;
   auto key_of = [&](int vk) { return LOCAL ? (vk < la ? vk : vk + rshift) : vk; };
   const size_t kvhead = ((size_t)b * a.Hkv + hkv) * (size_t)a.Skv;
-  const uint4* kp = reinterpret_cast<const uint4*>(a.k + kvhead * D) + dc;
-  const uint4* vp = reinterpret_cast<const uint4*>(a.v + kvhead * D) + dc;
+  // Buffer descriptors over the partition's rows (the whole head with a window,
+  // whose partitions map onto two runs of keys): a row past the range reads as
+  // zero without touching memory, so the loads need no clamping.
+  // Byte counts and offsets stay below 2^32: a head holds fewer than 2^31 elements.
+  const int rbase = LOCAL ? 0 : t0;
+  const unsigned rbytes = (unsigned)(LOCAL ? a.Skv : t1 - t0) * (2u * D);
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.k + (kvhead + rbase) * D), (short)0, (int)rbytes, kBufferFlags);
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.v + (kvhead + rbase) * D), (short)0, (int)rbytes, kBufferFlags);
   // Query rows of this kv head are contiguous: row r = g*Sq + sq.
   const size_t row0 = ((size_t)b * a.Hq + (size_t)hkv * a.G) * (size_t)a.Sq;
 
-  uint32_t qv[RMAX][4];
+  // Positive scale: a negative one is moved into q. The floor keeps a zero
+  // scale well defined (every visible key gets weight 1).
+  const float c = fmaxf(fabsf(a.c), 1e-30f);
+  const uint32_t qflip = a.c < 0.f ? 0x80008000u : 0u;
+  const float thr = kMoveThreshold / c;  // reference headroom in raw q.k units
+
+  u32x4_t qv[RMAX][CH];
   int lim[RMAX];
 #pragma unroll
   for (int r = 0; r < RMAX; ++r) {
     if (r < a.R) {
-      uint4 x = reinterpret_cast<const uint4*>(a.q + (row0 + r) * D)[dc];
-      qv[r][0] = x.x; qv[r][1] = x.y; qv[r][2] = x.z; qv[r][3] = x.w;
+      const u32x4_t* qp = reinterpret_cast<const u32x4_t*>(a.q + (row0 + r) * D) + dc;
+#pragma unroll
+      for (int i = 0; i < CH; ++i) qv[r][i] = qp[i * LPR] ^ qflip;
       lim[r] = a.causal ? (r % a.Sq) + a.Skv - a.Sq : 0x7fffffff;
     } else {
-      qv[r][0] = qv[r][1] = qv[r][2] = qv[r][3] = 0u;
+#pragma unroll
+      for (int i = 0; i < CH; ++i) qv[r][i] = u32x4_t{0u, 0u, 0u, 0u};
       lim[r] = -1;  // padding row: every key masked
     }
   }
+  // Whether every key of the partition is visible to every row (then only the
+  // ragged end of the partition needs the mask).
+  bool all_visible = !a.causal || a.Skv - a.Sq >= key_of(t1 - 1);
+  if constexpr (LOCAL) all_visible = all_visible && key_of(t0) >= a.Skv - a.runs.window;
+  all_visible = all_visible && a.R == RMAX;
 
-  float m[RMAX], l[RMAX], acc[RMAX][8];
+  float m[RMAX], nmc[RMAX], l[RMAX], acc[RMAX][DL];
 #pragma unroll
   for (int r = 0; r < RMAX; ++r) {
-    m[r] = kNegInf;
+    m[r] = kNegInf;  // reference, raw q.k units
+    nmc[r] = 0.f;    // -m * c (0 while m = -inf)
     l[r] = 0.f;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[r][e] = 0.f;
+    for (int e = 0; e < DL; ++e) acc[r][e] = 0.f;
   }
 
-  const float c = a.c;  // scale * log2(e): scores are kept in base-2 units
   constexpr int STEP = NW * TPL;  // key rows per workgroup-wide load
-  // Rows past the partition are clamped to its last row: the loads stay
-  // unconditional and the duplicates are masked out of the scores. The rows of
-  // the next iteration are requested before the current ones are used.
-  const int tlast = t1 - 1;
-  uint4 kn[U], vn[U];
-  if constexpr (PF) {
+  // Rows past the partition read as zero (their scores are masked).
+  auto load_set = [&](u32x4_t (&kr)[U][CH], u32x4_t (&vr)[U][CH], int tb) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int t = key_of(min(t0 + (u * NW + wave) * TPL + tl, tlast));
-      kn[u] = load16<NT>(kp + (size_t)t * LPR);
-      vn[u] = load16<NT>(vp + (size_t)t * LPR);
-    }
-  }
-  for (int tb = t0; tb < t1; tb += U * STEP) {
-    uint4 kr[U], vr[U];
-    int tok[U];
+      const int tok = tb + (u * NW + wave) * TPL + tl;
+      const unsigned row = LOCAL ? (tok < t1 ? key_of(tok) : a.Skv) : tok - t0;
+      const unsigned off = row * (2u * D) + dc * 16u;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      tok[u] = tb + (u * NW + wave) * TPL + tl;
-      if constexpr (PF) {
-        kr[u] = kn[u];
-        vr[u] = vn[u];
-      } else {
-        const int t = key_of(min(tok[u], tlast));
-        kr[u] = load16<NT>(kp + (size_t)t * LPR);
-        vr[u] = load16<NT>(vp + (size_t)t * LPR);
+      for (int i = 0; i < CH; ++i) {
+        kr[u][i] = __builtin_amdgcn_raw_buffer_load_b128(krs, off + i * LPR * 16, 0, kNonTemporal);
+        vr[u][i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, off + i * LPR * 16, 0, kNonTemporal);
       }
     }
-    if constexpr (PF) {
-      // Unconditional: past the end every row clamps to the partition's last row.
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int t = key_of(min(tb + U * STEP + (u * NW + wave) * TPL + tl, tlast));
-        kn[u] = load16<NT>(kp + (size_t)t * LPR);
-        vn[u] = load16<NT>(vp + (size_t)t * LPR);
-      }
-    }
-    // Scores in base-2 units, masked to -inf where the key is not visible.
+  };
+
+  auto consume = [&](const u32x4_t (&kr)[U][CH], const u32x4_t (&vr)[U][CH], int tb) {
+    // Raw scores q.k of this lane's key slots.
     float s[U][RMAX];
 #pragma unroll
     for (int u = 0; u < U; ++u) {
 #pragma unroll
       for (int r = 0; r < RMAX; ++r) {
-        float d = dot2_bf16(qv[r][0], kr[u].x, 0.f);
-        d = dot2_bf16(qv[r][1], kr[u].y, d);
-        d = dot2_bf16(qv[r][2], kr[u].z, d);
-        d = dot2_bf16(qv[r][3], kr[u].w, d);
-        d = group_sum<LPR>(d) * c;
-        const int key = key_of(tok[u]);
-        bool vis = tok[u] < t1 && key <= lim[r];
-        if constexpr (LOCAL) vis = vis && (key > lim[r] - a.runs.window || key < a.runs.sinks);
-        s[u][r] = vis ? d : kNegInf;
+        float d = 0.f;
+#pragma unroll
+        for (int i = 0; i < CH; ++i)
+#pragma unroll
+          for (int w = 0; w < 4; ++w) d = dot2_bf16(qv[r][i][w], kr[u][i][w], d);
+        s[u][r] = group_sum<LPR>(d);
       }
     }
-    float vf[U][8];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      vf[u][0] = bf16lo_to_f32(vr[u].x); vf[u][1] = bf16hi_to_f32(vr[u].x);
-      vf[u][2] = bf16lo_to_f32(vr[u].y); vf[u][3] = bf16hi_to_f32(vr[u].y);
-      vf[u][4] = bf16lo_to_f32(vr[u].z); vf[u][5] = bf16hi_to_f32(vr[u].z);
-      vf[u][6] = bf16lo_to_f32(vr[u].w); vf[u][7] = bf16hi_to_f32(vr[u].w);
-    }
-    // Rolling update: next_max, rescale of the carried state, new weights.
-#pragma unroll
-    for (int r = 0; r < RMAX; ++r) {
-      float bm = s[0][r];
-#pragma unroll
-      for (int u = 1; u < U; ++u) bm = fmaxf(bm, s[u][r]);
-      const float mn = fmaxf(m[r], bm);
-      const float ms = (mn == kNegInf) ? 0.f : mn;
-      const float rs = exp2_fast(m[r] - ms);
-      float psum = 0.f;
-      float pw[U];
+    if (!all_visible || tb + U * STEP > t1) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        pw[u] = exp2_fast(s[u][r] - ms);
-        psum += pw[u];
-      }
-      l[r] = l[r] * rs + psum;
+        const int tok = tb + (u * NW + wave) * TPL + tl;
+        const int key = key_of(tok);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        float x = acc[r][e] * rs;
-#pragma unroll
-        for (int u = 0; u < U; ++u) x = fmaf(pw[u], vf[u][e], x);
-        acc[r][e] = x;
+        for (int r = 0; r < RMAX; ++r) {
+          bool vis = tok < t1 && key <= lim[r];
+          if constexpr (LOCAL) vis = vis && (key > lim[r] - a.runs.window || key < a.runs.sinks);
+          s[u][r] = vis ? s[u][r] : kNegInf;
+        }
       }
-      m[r] = mn;
     }
-  }
-
-  // Merge the row groups of the wave (lanes l and l ^ LPR*k hold the same D slice).
-#pragma unroll
-  for (int off = LPR; off < 64; off <<= 1) {
+    // Reference update, only where a key exceeds the reference by the threshold.
+    float bm[RMAX];
+    bool up = false;
 #pragma unroll
     for (int r = 0; r < RMAX; ++r) {
-      const float mo = shfl_xor(m[r], off);
-      const float lo = shfl_xor(l[r], off);
-      const float mn = fmaxf(m[r], mo);
-      const float ms = (mn == kNegInf) ? 0.f : mn;
-      const float wa = exp2_fast(m[r] - ms), wb = exp2_fast(mo - ms);
-      l[r] = l[r] * wa + lo * wb;
+      bm[r] = s[0][r];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const float ao = shfl_xor(acc[r][e], off);
-        acc[r][e] = acc[r][e] * wa + ao * wb;
-      }
-      m[r] = mn;
+      for (int u = 1; u < U; ++u) bm[r] = fmaxf(bm[r], s[u][r]);
+      up = up || bm[r] > m[r] + thr;
     }
+    if (__builtin_amdgcn_ballot_w64(up)) {
+#pragma unroll
+      for (int r = 0; r < RMAX; ++r) {
+        const bool mv = bm[r] > m[r] + thr;
+        const float rs = mv ? exp2_fast((m[r] - bm[r]) * c) : 1.f;  // 0 when m = -inf
+        m[r] = mv ? bm[r] : m[r];
+        nmc[r] = (m[r] == kNegInf) ? 0.f : -m[r] * c;
+        l[r] *= rs;
+#pragma unroll
+        for (int e = 0; e < DL; ++e) acc[r][e] *= rs;
+      }
+    }
+    // Value elements of key pairs (u, u+1), shared by all rows.
+    uint32_t vlo[U / 2][CH][4], vhi[U / 2][CH][4];
+#pragma unroll
+    for (int h = 0; h < U / 2; ++h)
+#pragma unroll
+      for (int i = 0; i < CH; ++i)
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+          vlo[h][i][w] = pair_lo(vr[2 * h][i][w], vr[2 * h + 1][i][w]);
+          vhi[h][i][w] = pair_hi(vr[2 * h][i][w], vr[2 * h + 1][i][w]);
+        }
+#pragma unroll
+    for (int r = 0; r < RMAX; ++r) {
+#pragma unroll
+      for (int h = 0; h < U / 2; ++h) {
+        const float p0 = exp2_fast(fmaf(s[2 * h][r], c, nmc[r]));
+        const float p1 = exp2_fast(fmaf(s[2 * h + 1][r], c, nmc[r]));
+        l[r] += p0 + p1;
+        const uint32_t pk = pack_bf16x2(p0, p1);
+#pragma unroll
+        for (int i = 0; i < CH; ++i)
+#pragma unroll
+          for (int w = 0; w < 4; ++w) {
+            acc[r][i * 8 + 2 * w] = dot2_bf16(pk, vlo[h][i][w], acc[r][i * 8 + 2 * w]);
+            acc[r][i * 8 + 2 * w + 1] = dot2_bf16(pk, vhi[h][i][w], acc[r][i * 8 + 2 * w + 1]);
+          }
+      }
+    }
+  };
+
+  u32x4_t ka[U][CH], va[U][CH], kb[U][CH], vb[U][CH];
+  // Two sets of registers alternate: the rows of the next two steps are in
+  // flight while a step is used, each set reloaded right after its use. The
+  // scheduling barriers keep the first two sets in issue order, so the wait
+  // counts the loop relies on (the older set lands first) hold on entry as on
+  // every turn.
+  load_set(ka, va, t0);
+  __builtin_amdgcn_sched_barrier(0);
+  load_set(kb, vb, t0 + U * STEP);
+  __builtin_amdgcn_sched_barrier(0);
+  for (int tb = t0; tb < t1; tb += 2 * U * STEP) {
+    consume(ka, va, tb);
+    if (tb + U * STEP >= t1) break;
+    load_set(ka, va, tb + 2 * U * STEP);
+    consume(kb, vb, tb + U * STEP);
+    load_set(kb, vb, tb + 3 * U * STEP);
   }
+
+  // Reference in base-2 units of the scaled score for the merges below.
+#pragma unroll
+  for (int r = 0; r < RMAX; ++r) m[r] = (m[r] == kNegInf) ? kNegInf : m[r] * c;
+
+  // Merge the row groups of the wave: lanes LPR, 2 LPR, ... apart hold the same
+  // value elements of other keys.
+  auto merge_groups = [&](auto off_tag) {
+    constexpr int OFF = decltype(off_tag)::value;
+    if constexpr (OFF < 64) {
+#pragma unroll
+      for (int r = 0; r < RMAX; ++r) {
+        float ma, mb, la_, lb;
+        lane_pair<OFF>(m[r], ma, mb);
+        lane_pair<OFF>(l[r], la_, lb);
+        const float mn = fmaxf(ma, mb);
+        const float ms = (mn == kNegInf) ? 0.f : mn;
+        const float wa = exp2_fast(ma - ms), wb = exp2_fast(mb - ms);
+        l[r] = la_ * wa + lb * wb;
+#pragma unroll
+        for (int e = 0; e < DL; ++e) {
+          float xa, xb;
+          lane_pair<OFF>(acc[r][e], xa, xb);
+          acc[r][e] = xa * wa + xb * wb;
+        }
+        m[r] = mn;
+      }
+    }
+  };
+  merge_groups(std::integral_constant<int, LPR>{});
+  merge_groups(std::integral_constant<int, 2 * LPR>{});
+  merge_groups(std::integral_constant<int, 4 * LPR>{});
+  merge_groups(std::integral_constant<int, 8 * LPR>{});
 
   // Merge the waves through LDS and store the partition's state.
   __shared__ float sm[NW][RMAX], sl[NW][RMAX];
@@ -189,7 +280,9 @@ __global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
         sl[wave][r] = l[r];
       }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) sacc[wave][r][dc * 8 + e] = acc[r][e];
+      for (int i = 0; i < CH; ++i)
+#pragma unroll
+        for (int e = 0; e < 8; ++e) sacc[wave][r][(dc + i * LPR) * 8 + e] = acc[r][i * 8 + e];
     }
   }
   __syncthreads();
@@ -230,39 +323,39 @@ __global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
     __shared__ float cw[RMAX * kFusedMaxP];
     __shared__ float cl[RMAX * kFusedMaxP];
     __shared__ float cinv[RMAX];
-    if (!last_of_group(a.counters + (size_t)b * a.Hkv + hkv, P)) return;
+    unsigned* counter = a.counters + ((size_t)b * a.Hkv + hkv) * kCounterStride;
+    if (!last_of_group(counter, P)) return;
     combine_group<D, NW * 64>(a.ws_m, a.ws_l, a.ws_acc, a.o, row0, a.R, P, cw, cl, cinv);
-    if (threadIdx.x == 0) reset_counter(a.counters + (size_t)b * a.Hkv + hkv);
+    if (threadIdx.x == 0) reset_counter(counter);
   }
 }
 
-// Launch shape by grid size (measured on the GQA decode and 131072-key
-// workloads); local attention (window > 0) selects the variant that maps
-// virtual keys onto the sink and window runs: a grid that fits the chip in one round runs best with 2-wave
-// workgroups that request their next rows before using the current ones; a
-// grid several rounds deep runs best with 4-wave workgroups and no prefetch.
+template <int D, int RMAX, int NW, int U, int CH, bool FUSED, bool LOCAL>
+__global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
+  decode_partition<D, RMAX, NW, U, CH, FUSED, LOCAL>(a, blockIdx.x, blockIdx.y, blockIdx.z);
+}
+
+// Launch shape per row count, measured on one-token decode with 1024
+// workgroups of 256-key partitions (G = 1, 2, 4, 8) and on the 131072-key
+// decode: one 16-byte chunk per lane and key row (16 lanes per row at
+// D = 128; two chunks per lane cost more than the shorter reductions save),
+// and the waves per workgroup and key slots per lane that ran fastest.
+template <int RMAX>
+constexpr int kWaves = (RMAX == 1 || RMAX == 4) ? 1 : 2;
+template <int RMAX>
+constexpr int kSlots = RMAX <= 2 ? 4 : 2;
+
 template <int D, int RMAX, bool LOCAL>
 static hipError_t launch_decode_rl(const DecodeParams& a, hipStream_t stream) {
-  constexpr int U = RMAX <= 2 ? 4 : 2;
-  const long long blocks = (long long)a.P * a.Hkv * a.B;
+  constexpr int NW = kWaves<RMAX>;
+  constexpr int U = kSlots<RMAX>;
   dim3 grid(a.P, a.Hkv, a.B);
-  const bool fused = a.counters != nullptr;
-  if (blocks <= 2048) {
-    if (fused) {
-      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 2, U, true, true, true, LOCAL>), grid,
-                         dim3(2 * 64), 0, stream, a);
-    } else {
-      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 2, U, true, true, false, LOCAL>), grid,
-                         dim3(2 * 64), 0, stream, a);
-    }
+  if (a.counters != nullptr) {
+    hipLaunchKernelGGL((decode_split_kernel<D, RMAX, NW, U, 1, true, LOCAL>), grid, dim3(NW * 64),
+                       0, stream, a);
   } else {
-    if (fused) {
-      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 4, U, false, true, true, LOCAL>), grid,
-                         dim3(4 * 64), 0, stream, a);
-    } else {
-      hipLaunchKernelGGL((decode_split_kernel<D, RMAX, 4, U, false, true, false, LOCAL>), grid,
-                         dim3(4 * 64), 0, stream, a);
-    }
+    hipLaunchKernelGGL((decode_split_kernel<D, RMAX, NW, U, 1, false, LOCAL>), grid,
+                       dim3(NW * 64), 0, stream, a);
   }
   return hipGetLastError();
 }

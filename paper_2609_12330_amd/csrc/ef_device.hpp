@@ -69,14 +69,14 @@ constexpr int kDppHalfMirror = 0x141;
 constexpr int kDppQuadXor2 = 0x4e;  // quad_perm [2,3,0,1]
 constexpr int kDppQuadXor1 = 0xb1;  // quad_perm [1,0,3,2]
 
-// Sum over aligned groups of LANES lanes (16 or 8); every lane gets the group's sum.
+// Sum over aligned groups of LANES lanes (16, 8 or 4); every lane gets the group's sum.
 template <int LANES>
 __device__ __forceinline__ float group_sum(float x) {
-  static_assert(LANES == 16 || LANES == 8, "group of 8 or 16 lanes");
+  static_assert(LANES == 16 || LANES == 8 || LANES == 4, "group of 4, 8 or 16 lanes");
   if constexpr (LANES == 16) {
     x += dpp_mov<kDppRowRor8>(x);
     x += dpp_mov<kDppRowRor4>(x);
-  } else {
+  } else if constexpr (LANES == 8) {
     x += dpp_mov<kDppHalfMirror>(x);
   }
   x += dpp_mov<kDppQuadXor2>(x);
@@ -86,6 +86,31 @@ __device__ __forceinline__ float group_sum(float x) {
 
 __device__ __forceinline__ float shfl_xor(float x, int mask) {
   return __shfl_xor(x, mask, 64);
+}
+
+// The values of x in this lane and in its partner lane at distance OFF, as a
+// pair (a, b) whose order may differ between the two lanes. OFF = 16 and 32
+// pair lane l with l ^ OFF (permlane swaps); OFF = 4 and 8 pair lane l with
+// lane l + OFF of its 16-lane row (DPP rotation; for 8 that is l ^ 8). Taking
+// OFF = 4, 8, 16, 32 in increasing order from some start combines every lane
+// group, like a butterfly.
+template <int OFF>
+__device__ __forceinline__ void lane_pair(float x, float& a, float& b) {
+  static_assert(OFF == 4 || OFF == 8 || OFF == 16 || OFF == 32, "lane distance");
+  if constexpr (OFF == 4 || OFF == 8) {
+    a = x;
+    b = dpp_mov<OFF == 4 ? kDppRowRor4 : kDppRowRor8>(x);
+  } else if constexpr (OFF == 16) {
+    const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+    a = __uint_as_float(r[0]);
+    b = __uint_as_float(r[1]);
+  } else {
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false,
+                                                    false);
+    a = __uint_as_float(r[0]);
+    b = __uint_as_float(r[1]);
+  }
 }
 
 // Partial-state workspace: m [rows][P], l [rows][P], acc [rows][P][D] fp32.

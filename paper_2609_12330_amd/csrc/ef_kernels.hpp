@@ -41,6 +41,10 @@ struct DecodeParams {
 // Largest partition count for which the producer combines its group itself.
 constexpr int kFusedMaxP = 64;
 
+// Arrival counters sit 256 bytes apart (one counter per (batch, kv head)):
+// counters sharing a line serialise the workgroups' arrivals at the end.
+constexpr int kCounterStride = 64;
+
 // MFMA attention (single pass, or split producer when ws_m != nullptr).
 struct MfmaParams {
   const uint16_t* q;

@@ -44,14 +44,73 @@ __device__ __forceinline__ void reset_counter(unsigned* counter) {
   __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// 16 bytes from byte offset `off` of a buffer, read at device scope (coherent
+// across XCDs: the read does not hit a stale line of this XCD's L2); 0 when
+// `off` is past the buffer.
+__device__ __forceinline__ u32x4_t load16_dev(__amdgpu_buffer_rsrc_t rs, int off) {
+  constexpr int kDeviceScope = 16;  // sc1 cache policy
+  return __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, kDeviceScope);
+}
+
 // o[row0 + r][:] = sum_p exp(m_p - M) acc_p / sum_p exp(m_p - M) l_p over the
 // P stored states of rows row0 .. row0 + nrows - 1 (0 for a row with no
 // visible key), the states read with device-scope loads. cw, cl: LDS of at
-// least nrows * P floats; cinv: nrows floats.
+// least nrows * P floats; cinv: nrows floats. The combine is the tail of the
+// producer that arrives last, so it is arranged for few round trips: each
+// thread owns two 4-element slices of the output rows and requests the value
+// states of 16 partitions of both at once, the first 16 together with the
+// reference points and sums.
 template <int D, int NT>
-__device__ void combine_group(const float* ws_m, const float* ws_l, const float* ws_acc, float* o,
-                              size_t row0, int nrows, int P, float* cw, float* cl, float* cinv) {
+__device__ __forceinline__ void combine_group(const float* ws_m, const float* ws_l,
+                                              const float* ws_acc, float* o, size_t row0,
+                                              int nrows, int P, float* cw, float* cl,
+                                              float* cinv) {
+  constexpr int D4 = D / 4;  // 4-element slices of a row
+  constexpr int BATCH = 16;  // partitions per slice in flight
   const int n = nrows * P;
+  const int bytes = n * D * 4;  // at most 8 * 64 * 128 * 4
+  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(ws_acc + row0 * (size_t)P * D), (short)0, bytes, 0x00020000);
+  const int nslices = nrows * D4;
+
+  // Byte offset of slice c's value state in partition p; the buffer's end (a
+  // zero read) past the row's partitions or past the slices.
+  auto slice_off = [&](int c, int p) {
+    return (c < nslices && p < P) ? ((c / D4) * P * D + p * D + (c % D4) * 4) * 4 : bytes;
+  };
+  auto load_batch = [&](int c0, int p0, u32x4_t (&x0)[BATCH], u32x4_t (&x1)[BATCH]) {
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j) {
+      x0[j] = load16_dev(rs, slice_off(c0, p0 + j));
+      x1[j] = load16_dev(rs, slice_off(c0 + NT, p0 + j));
+    }
+  };
+  auto fold_batch = [&](int c0, int p0, const u32x4_t (&x0)[BATCH], const u32x4_t (&x1)[BATCH],
+                        floatx4& s0, floatx4& s1) {
+    const int r0 = min(c0, nslices - 1) / D4, r1 = min(c0 + NT, nslices - 1) / D4;
+#pragma unroll
+    for (int j = 0; j < BATCH; ++j) {
+      const int p = min(p0 + j, P - 1);
+      const float w0 = p0 + j < P ? cw[r0 * P + p] : 0.f;
+      const float w1 = p0 + j < P ? cw[r1 * P + p] : 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        s0[e] = fmaf(w0, __uint_as_float(x0[j][e]), s0[e]);
+        s1[e] = fmaf(w1, __uint_as_float(x1[j][e]), s1[e]);
+      }
+    }
+  };
+  auto store_slice = [&](int c, const floatx4& sv) {
+    if (c < nslices) {
+      const float inv = cinv[c / D4];
+      *reinterpret_cast<float4*>(o + (row0 + c / D4) * D + (c % D4) * 4) =
+          make_float4(sv[0] * inv, sv[1] * inv, sv[2] * inv, sv[3] * inv);
+    }
+  };
+
+  u32x4_t x0[BATCH], x1[BATCH];
+  load_batch(threadIdx.x, 0, x0, x1);  // first values in flight with the m, l reads
+#pragma unroll 8
   for (int i = threadIdx.x; i < n; i += NT) {
     cw[i] = load_dev(ws_m + row0 * P + i);
     cl[i] = load_dev(ws_l + row0 * P + i);
@@ -70,17 +129,16 @@ __device__ void combine_group(const float* ws_m, const float* ws_l, const float*
     cinv[r] = (M == kNegInf || L == 0.f) ? 0.f : 1.f / L;
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < nrows * D; i += NT) {
-    const int r = i / D, d = i % D;
-    const float* ap = ws_acc + (row0 + r) * (size_t)P * D + d;
-    float s0 = 0.f, s1 = 0.f;
-    int p = 0;
-    for (; p + 1 < P; p += 2) {
-      s0 = fmaf(cw[r * P + p], load_dev(ap + (size_t)p * D), s0);
-      s1 = fmaf(cw[r * P + p + 1], load_dev(ap + (size_t)(p + 1) * D), s1);
+  for (int c0 = threadIdx.x; c0 < nslices; c0 += 2 * NT) {
+    floatx4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
+    if (c0 != (int)threadIdx.x) load_batch(c0, 0, x0, x1);
+    fold_batch(c0, 0, x0, x1, s0, s1);
+    for (int p0 = BATCH; p0 < P; p0 += BATCH) {
+      load_batch(c0, p0, x0, x1);
+      fold_batch(c0, p0, x0, x1, s0, s1);
     }
-    if (p < P) s0 = fmaf(cw[r * P + p], load_dev(ap + (size_t)p * D), s0);
-    o[(row0 + r) * D + d] = (s0 + s1) * cinv[r];
+    store_slice(c0, s0);
+    store_slice(c0 + NT, s1);
   }
 }
 

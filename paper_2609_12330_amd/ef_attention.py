@@ -291,13 +291,14 @@ def workspace_views(ws, B, Hq, Sq, Skv, D, T, window=0, sinks=0):
 
 
 def workspace_counters(ws, B, Hq, Hkv, Sq, Skv, D, T, window=0, sinks=0):
-    """int32 view of the per-(batch, kv head) arrival counters of a split-KV workspace."""
+    """int32 view [B*Hkv, 64] of the arrival-counter slots of a split-KV workspace (word 0
+    of each slot is the counter of one (batch, kv head))."""
     torch = _torch()
     rows = B * Hq * Sq
     P = splitkv_partitions(Sq, Skv, T, window, sinks)
     a = (rows * P * 4 + 255) // 256 * 256
     c = (2 * a + rows * P * D * 4 + 255) // 256 * 256
-    return ws[c: c + 4 * B * Hkv].view(torch.int32)
+    return ws[c: c + 256 * B * Hkv].view(torch.int32).view(B * Hkv, 64)
 
 
 def attention_splitkv(q, k, v, scale: Optional[float] = None, causal: bool = False,

@@ -174,7 +174,7 @@ def test_workspace_and_partition_arithmetic():
     def layout(rows, P, D, kv_heads):
         a = (rows * P * 4 + 255) // 256 * 256
         c = (2 * a + rows * P * D * 4 + 255) // 256 * 256
-        return c + kv_heads * 4
+        return c + kv_heads * 256
 
     # GQA decode, 256-key partitions: rows = 8*32, P = 16, 64 kv heads
     assert ws(8, 32, 8, 1, 4096, 128, 256) == layout(256, 16, 128, 64)
@@ -198,7 +198,7 @@ def test_workspace_and_partition_arithmetic():
 def _layout(rows, P, D, kv_heads):
     a = (rows * P * 4 + 255) // 256 * 256
     c = (2 * a + rows * P * D * 4 + 255) // 256 * 256
-    return c + kv_heads * 4
+    return c + kv_heads * 256
 
 
 def _runs(Sq, Skv, W, S):
