@@ -21,15 +21,13 @@
 // scores into weights, the matrix core already computes tile j+1's scores,
 // then tile j's values are multiplied. K is therefore staged one tile ahead
 // of V: during step j, K stage (j+1)%2 holds K of tile j+1 and V stage j%2
-// holds V of tile j, and the step writes K of tile j+2 and V of tile j+1 into
+// holds V of tile j, and the step loads K of tile j+2 and V of tile j+1 into
 // the two stages nobody reads during it, so one workgroup barrier per tile
-// suffices. Tiles go HBM -> registers -> LDS; each tile's buffer loads use a
-// descriptor covering exactly the workgroup's remaining key range, so rows
-// past it read as zero (no clamping or predication, and a tile after the last
-// one reads nothing). K is stored row-major and V transposed (V^T, keys
-// permuted so each lane's 8 keys of a P^T fragment are contiguous), both in
-// rows padded by 16 bytes, which keeps the fragment reads free of bank
-// conflicts while every LDS address is a per-lane base plus an immediate.
+// suffices. Tiles go from HBM straight into LDS (direct loads, no staging
+// registers), row-major with their 16-byte chunks permuted per row so that
+// the fragment reads are free of bank conflicts. The V^T operand of the
+// second product comes from transposing LDS reads (ds_read_b64_tr_b16) of the
+// row-major V tile, in the key order of the P^T fragments.
 //
 // The maximum used as the exponent reference is only moved up when a tile's
 // maximum exceeds it by more than 8 (base-2 units), so the carried sum and
@@ -55,41 +53,33 @@ namespace {
 
 constexpr int BN = 64;                 // keys per tile
 constexpr float kLazyThreshold = 8.f;  // base-2 headroom before the reference moves
-constexpr uint32_t kBufferFlags = 0x00020000u;  // raw 32-bit buffer access
 constexpr unsigned kXcds = 8;                   // accelerator dies of the chip
 
 template <int D>
 struct TileGeom {
-  static constexpr int KCH = D / 8;               // 16-byte chunks per K row
-  static constexpr int K_STRIDE = 2 * D + 16;     // padded K row, bytes
-  static constexpr int V_STRIDE = 2 * BN + 16;    // padded V^T row, bytes
-  static constexpr int K_BYTES = BN * K_STRIDE;
-  static constexpr int V_BYTES = D * V_STRIDE;
-  // LDS: V^T stage 0, V^T stage 1, K stage 0, K stage 1 (all immediates < 64 KiB).
+  static constexpr int KCH = D / 8;        // 16-byte chunks per row
+  static constexpr int ROW = 2 * D;        // bytes per K or V row (no padding: swizzled)
+  static constexpr int RPI = 64 / KCH;     // rows one wave-wide direct load fills
+  static constexpr int TILE_BYTES = BN * ROW;
+  // LDS: V stage 0, V stage 1, K stage 0, K stage 1 (all immediates < 64 KiB).
   static constexpr int V_OFF0 = 0;
-  static constexpr int V_OFF1 = V_BYTES;
-  static constexpr int K_OFF0 = 2 * V_BYTES;
-  static constexpr int K_OFF1 = 2 * V_BYTES + K_BYTES;
-  static constexpr int LDS_BYTES = 2 * (K_BYTES + V_BYTES);
+  static constexpr int V_OFF1 = TILE_BYTES;
+  static constexpr int K_OFF0 = 2 * TILE_BYTES;
+  static constexpr int K_OFF1 = 3 * TILE_BYTES;
+  static constexpr int LDS_BYTES = 4 * TILE_BYTES;
   template <int S>
   static constexpr int v_off() { return S == 0 ? V_OFF0 : V_OFF1; }
   template <int S>
   static constexpr int k_off() { return S == 0 ? K_OFF0 : K_OFF1; }
+  // Tiles sit row-major in LDS with their 16-byte chunks permuted per row
+  // (chunk c of row r at slot c ^ swz(r)), so the fragment reads below hit
+  // distinct banks: K rows are read 16 rows at a time at one chunk, V rows four
+  // rows at a time at 32 consecutive bytes (transposing reads).
+  static __device__ __forceinline__ int swz_k(int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); }
+  static __device__ __forceinline__ int swz_v(int r) {
+    return D == 128 ? 4 * (r & 3) : 4 * ((r >> 1) & 1);
+  }
 };
-
-// Slot of key kappa (0..63) inside a V^T row: swap bits 2 and 3 of kappa.
-__device__ __forceinline__ int vslot(int kappa) {
-  return (kappa & ~12) | ((kappa & 4) << 1) | ((kappa & 8) >> 1);
-}
-
-// Descriptor over the rows [0, rows) of a tile starting at `base`; only the
-// tile's own BN rows are ever read through it, so it covers at most those.
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_over(const uint16_t* base, int rows,
-                                                              int row_bytes) {
-  const int bytes = rows > 0 ? min(rows, BN) * row_bytes : 0;
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base), (short)0, bytes,
-                                           kBufferFlags);
-}
 
 // Cross-half exchange: max of x over lanes l and l ^ 32.
 __device__ __forceinline__ float max_with_other_half(float x) {
@@ -118,91 +108,57 @@ struct TileList {
   }
 };
 
+// Tiles go straight from HBM to LDS (one 16-byte chunk per lane and load,
+// each wave-wide load filling RPI whole rows): no staging registers and no
+// LDS stores. Rows past the tile's run repeat its last row (their keys are
+// masked, their values finite); a tile past the last one loads nothing.
 template <int D, int NW>
 struct Loader {
   using G = TileGeom<D>;
-  static constexpr int NT = NW * 64;
-  static constexpr int K_CHUNKS = BN * G::KCH;        // 16-byte chunks per K tile
-  static constexpr int K_PER_T = K_CHUNKS / NT;       // per thread
-  static constexpr int V_GROUPS = (BN / 4) * G::KCH;  // (4 keys x 8 d) groups per V tile
-  static constexpr int V_PER_T = (V_GROUPS + NT - 1) / NT;
-  static_assert(K_CHUNKS % NT == 0, "K tile split");
-  static_assert(V_GROUPS % NT == 0 || NT % V_GROUPS == 0, "V tile split");
-
-  u32x4_t kreg[K_PER_T];
-  u32x4_t vreg[V_PER_T][4];
-  int kvoff[K_PER_T];  // byte offset of this thread's K chunk inside the tile
-  int vvoff[V_PER_T];  // byte offset of this thread's first V row chunk inside the tile
-  int kst[K_PER_T];    // LDS byte offset of the K chunk inside a K stage
-  int vst[V_PER_T];    // LDS byte offset of the V^T group inside a V stage
-  bool vact[V_PER_T];
+  static constexpr int INSTS = BN / G::RPI / NW;  // direct loads per wave and tile
+  static_assert(INSTS * G::RPI * NW == BN, "tile split over the waves");
+  int row[INSTS];     // tile row whose chunk this lane loads
+  int kchunk[INSTS];  // element offset of that chunk in a K row
+  int vchunk[INSTS];  // element offset of that chunk in a V row
+  int wave;
 
   __device__ __forceinline__ void init() {
-    const int t = threadIdx.x;
+    const int lane = threadIdx.x & 63;
+    wave = threadIdx.x >> 6;
 #pragma unroll
-    for (int i = 0; i < K_PER_T; ++i) {
-      const int id = t + i * NT;
-      const int row = id / G::KCH, ch = id % G::KCH;
-      kvoff[i] = row * (2 * D) + ch * 16;
-      kst[i] = row * G::K_STRIDE + ch * 16;
-    }
-#pragma unroll
-    for (int i = 0; i < V_PER_T; ++i) {
-      // 16 consecutive threads take the 16 key quads of one 8-column chunk, so each
-      // of their transposed stores fills one V^T row's 128 bytes.
-      const int gid = t + i * NT;
-      vact[i] = gid < V_GROUPS;
-      const int kq = gid % 16, ch = (gid / 16) % G::KCH;
-      vvoff[i] = kq * 4 * (2 * D) + ch * 16;
-      vst[i] = ch * 8 * G::V_STRIDE + vslot(kq * 4) * 2;
+    for (int i = 0; i < INSTS; ++i) {
+      const int blk = wave + NW * i;
+      row[i] = blk * G::RPI + lane / G::KCH;
+      const int slot = lane % G::KCH;
+      kchunk[i] = (slot ^ G::swz_k(row[i])) * 8;
+      vchunk[i] = (slot ^ G::swz_v(row[i])) * 8;
     }
   }
 
-  // Tile loads through a descriptor covering [kb, kend) of this head's K or V.
-  __device__ __forceinline__ void load_k(const uint16_t* kh, int kb, int kend) {
-    const __amdgpu_buffer_rsrc_t rk = buffer_over(kh + (size_t)kb * D, kend - kb, 2 * D);
+  template <bool ISK>
+  __device__ __forceinline__ void load(char* stage, const uint16_t* head, int kb, int kend) const {
+    const int nrows = kend - kb;
+    if (nrows <= 0) return;
 #pragma unroll
-    for (int i = 0; i < K_PER_T; ++i)
-      kreg[i] = __builtin_amdgcn_raw_buffer_load_b128(rk, kvoff[i], 0, 0);
-  }
-  __device__ __forceinline__ void load_v(const uint16_t* vh, int kb, int kend) {
-    const __amdgpu_buffer_rsrc_t rv = buffer_over(vh + (size_t)kb * D, kend - kb, 2 * D);
-#pragma unroll
-    for (int i = 0; i < V_PER_T; ++i)
-#pragma unroll
-      for (int x = 0; x < 4; ++x)
-        vreg[i][x] = __builtin_amdgcn_raw_buffer_load_b128(rv, vvoff[i] + x * 2 * D, 0, 0);
-  }
-
-  template <int S>
-  __device__ __forceinline__ void store_k(char* smem) const {
-#pragma unroll
-    for (int i = 0; i < K_PER_T; ++i)
-      *reinterpret_cast<u32x4_t*>(smem + G::template k_off<S>() + kst[i]) = kreg[i];
-  }
-  template <int S>
-  __device__ __forceinline__ void store_v(char* smem) const {
-#pragma unroll
-    for (int i = 0; i < V_PER_T; ++i) {
-      if constexpr (V_GROUPS % NT != 0) {
-        if (!vact[i]) break;
-      }
-      const u32x4_t x0 = vreg[i][0], x1 = vreg[i][1], x2 = vreg[i][2], x3 = vreg[i][3];
-#pragma unroll
-      for (int w = 0; w < 4; ++w) {
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          const uint32_t sel = half ? 0x07060302u : 0x05040100u;
-          u32x2_t val;
-          val[0] = __builtin_amdgcn_perm(x1[w], x0[w], sel);  // keys 0,1 at column d
-          val[1] = __builtin_amdgcn_perm(x3[w], x2[w], sel);  // keys 2,3 at column d
-          *reinterpret_cast<u32x2_t*>(smem + G::template v_off<S>() + vst[i] +
-                                      (w * 2 + half) * G::V_STRIDE) = val;
-        }
-      }
+    for (int i = 0; i < INSTS; ++i) {
+      const int r = min(row[i], nrows - 1);
+      const uint16_t* g = head + (size_t)(kb + r) * D + (ISK ? kchunk[i] : vchunk[i]);
+      char* l = stage + (wave + NW * i) * 1024;
+      __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)l, 16, 0, 0);
     }
+  }
+  template <int S>
+  __device__ __forceinline__ void load_k(char* smem, const uint16_t* kh, int kb, int kend) const {
+    load<true>(smem + G::template k_off<S>(), kh, kb, kend);
+  }
+  template <int S>
+  __device__ __forceinline__ void load_v(char* smem, const uint16_t* vh, int kb, int kend) const {
+    load<false>(smem + G::template v_off<S>(), vh, kb, kend);
   }
 };
+
+// Waits for this wave's direct-to-LDS loads (they count as vector memory loads).
+__device__ __forceinline__ void wait_tile_loads() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 
 // Occupancy target: two waves per SIMD for 4-wave workgroups (two workgroups per
 // CU overlap each other's barrier and memory stalls); the 2-wave variant keeps
@@ -218,7 +174,7 @@ struct Tile {
 
   // S^T of the key tile in K stage S: two 32-key halves, 16-deep MFMA k-steps.
   template <int S>
-  static __device__ __forceinline__ void scores(const char* smem, int kbase_lane,
+  static __device__ __forceinline__ void scores(const char* smem, const int* kread,
                                                 const bf16x8_t* qf, floatx16* sacc) {
 #pragma unroll
     for (int half = 0; half < 2; ++half)
@@ -229,7 +185,7 @@ struct Tile {
 #pragma unroll
       for (int half = 0; half < 2; ++half) {
         const u32x4_t kx = *reinterpret_cast<const u32x4_t*>(
-            smem + Geo::template k_off<S>() + kbase_lane + half * 32 * Geo::K_STRIDE + s * 32);
+            smem + Geo::template k_off<S>() + kread[s] + half * 32 * Geo::ROW);
         sacc[half] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kx),
                                                             qf[s], sacc[half], 0, 0, 0);
       }
@@ -240,26 +196,29 @@ struct Tile {
   // rolling reference update; returns -reference (0 while nothing is visible).
   // A key is hidden from this lane's row when it is past the tile's run, past
   // the causal limit `lim`, or at most `lo` (left of the window) and not a sink.
-  static __device__ __forceinline__ float prepare(floatx16* sacc, float* x, floatx16* oacc,
-                                                  float& lsum, float& mref, float c, int kb,
-                                                  int kend, bool masked, int lim, int lo,
-                                                  int sinks, int h) {
+  // The scores are rewritten in place.
+  static __device__ __forceinline__ float prepare(floatx16* x, floatx16* oacc, float& lsum,
+                                                  float& mref, float c, int kb, int kend,
+                                                  bool masked, int lim, int lo, int sinks,
+                                                  int h) {
+    if constexpr (NEG) {
 #pragma unroll
-    for (int half = 0; half < 2; ++half)
+      for (int half = 0; half < 2; ++half)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) x[half * 16 + i] = NEG ? -sacc[half][i] : sacc[half][i];
+        for (int i = 0; i < 16; ++i) x[half][i] = -x[half][i];
+    }
     if (masked) {
 #pragma unroll
       for (int half = 0; half < 2; ++half)
 #pragma unroll
         for (int i = 0; i < 16; ++i) {
           const int key = kb + half * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-          if (key >= kend || key > lim || (key <= lo && key >= sinks)) x[half * 16 + i] = kNegInf;
+          if (key >= kend || key > lim || (key <= lo && key >= sinks)) x[half][i] = kNegInf;
         }
     }
-    float tmax = fmaxf(x[0], x[1]);
+    float tmax = fmaxf(x[0][0], x[0][1]);
 #pragma unroll
-    for (int i = 2; i < 32; ++i) tmax = fmaxf(tmax, x[i]);
+    for (int i = 2; i < 32; ++i) tmax = fmaxf(tmax, x[i >> 4][i & 15]);
     tmax = max_with_other_half(tmax);
     const float cand = tmax * c;  // tile maximum in base-2 units (c > 0)
     // Move the reference only when the tile exceeds it by the threshold.
@@ -276,25 +235,30 @@ struct Tile {
     return (mref == kNegInf) ? 0.f : -mref;
   }
 
-  // Weights 2^(x*c - reference) as bf16 pairs (P^T fragments) and their row sum.
-  static __device__ __forceinline__ void weights(const float* x, float c, float mneg,
+  // Weights 2^(x*c - reference) as bf16 pairs (P^T fragments) and their row
+  // sum, taken over the rounded weights the value product uses (one packed
+  // dot product with (1, 1) per pair).
+  static __device__ __forceinline__ void weights(const floatx16* x, float c, float mneg,
                                                  uint32_t* pk, float& lsum) {
-    float ps0 = 0.f, ps1 = 0.f;
+    constexpr uint32_t kOnes = 0x3f803f80u;  // bf16 pair (1, 1)
+    float ps[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      const float p0 = exp2_fast(fmaf(x[2 * i], c, mneg));
-      const float p1 = exp2_fast(fmaf(x[2 * i + 1], c, mneg));
-      ps0 += p0;
-      ps1 += p1;
+      const float p0 = exp2_fast(fmaf(x[(2 * i) >> 4][(2 * i) & 15], c, mneg));
+      const float p1 = exp2_fast(fmaf(x[(2 * i + 1) >> 4][(2 * i + 1) & 15], c, mneg));
       pk[i] = pack_bf16x2(p0, p1);
+      ps[i & 3] = dot2_bf16(pk[i], kOnes, ps[i & 3]);
     }
-    lsum += ps0 + ps1;
+    lsum += (ps[0] + ps[1]) + (ps[2] + ps[3]);
   }
 
-  // O^T += V^T * P^T over the four 16-key steps of the tile in V stage S.
+  // O^T += V^T * P^T over the four 16-key steps of the tile in V stage S. The
+  // V^T operand (8 keys of one value column per lane) comes from two
+  // transposing reads of 4 keys each out of the row-major V tile.
   template <int S>
-  static __device__ __forceinline__ void values(const char* smem, int vbase_lane,
+  static __device__ __forceinline__ void values(const char* smem, const int* vread,
                                                 const uint32_t* pk, floatx16* oacc) {
+    typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
       // P^T fragment: registers 8*(s%2) .. +8 of score half s/2, i.e. pk[4*s .. 4*s+3].
@@ -302,38 +266,42 @@ struct Tile {
       const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pv);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const u32x4_t vx = *reinterpret_cast<const u32x4_t*>(
-            smem + Geo::template v_off<S>() + vbase_lane + dt * 32 * Geo::V_STRIDE + s * 32);
-        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vx), pf,
-                                                          oacc[dt], 0, 0, 0);
+        const char* p = smem + Geo::template v_off<S>() + vread[dt] + 16 * s * Geo::ROW;
+        const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (__attribute__((address_space(3))) bf16x4_t*)(p));
+        const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+            (__attribute__((address_space(3))) bf16x4_t*)(p + 8 * Geo::ROW));
+        const bf16x8_t vx = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vx, pf, oacc[dt], 0, 0, 0);
       }
     }
   }
 };
 
-// One pipelined step on tile j (stage parity S = j % 2). On entry sacc holds
+// One pipelined step on tile j (stage parity S = j % 2). On entry sacc[S] holds
 // S^T of tile j, K stage 1-S holds tile j+1 and V stage S holds tile j. The
-// step computes tile j's weights while the matrix core computes tile j+1's
-// scores, multiplies tile j's values, and stages K of tile j+2 (into K stage
-// S, last read for tile j's scores) and V of tile j+1 (into V stage 1-S, last
-// read for tile j-1's values) before the workgroup barrier.
+// step requests K of tile j+2 (into K stage S, last read for tile j's scores)
+// and V of tile j+1 (into V stage 1-S, last read for tile j-1's values)
+// straight into LDS, computes tile j's weights while the matrix core computes
+// tile j+1's scores, multiplies tile j's values, and waits for its loads
+// before the workgroup barrier.
 template <int D, int NW, bool NEG, int S>
 __device__ __forceinline__ void pipelined_step(
-    char* smem, Loader<D, NW>& ld, const uint16_t* kh, const uint16_t* vh, const TileList& tl,
-    int j, int lim, int lo, int h, int kbase_lane, int vbase_lane, const bf16x8_t* qf,
-    floatx16* sacc, floatx16* oacc, float& lsum, float& mref, float c) {
+    char* smem, const Loader<D, NW>& ld, const uint16_t* kh, const uint16_t* vh,
+    const TileList& tl, int j, int lim, int lo, int h, const int* kread, const int* vread,
+    const bf16x8_t* qf, floatx16 (*sacc)[2], floatx16* oacc, float& lsum, float& mref,
+    float c) {
   using TileT = Tile<D, NEG>;
-  ld.load_k(kh, tl.base(j + 2), tl.end(j + 2));  // past the last tile nothing is covered
-  ld.load_v(vh, tl.base(j + 1), tl.end(j + 1));
-  float x[32];
-  const float mneg = TileT::prepare(sacc, x, oacc, lsum, mref, c, tl.base(j), tl.end(j),
+  ld.template load_k<S>(smem, kh, tl.base(j + 2), tl.end(j + 2));  // nothing past the last tile
+  ld.template load_v<1 - S>(smem, vh, tl.base(j + 1), tl.end(j + 1));
+  const float mneg = TileT::prepare(sacc[S], oacc, lsum, mref, c, tl.base(j), tl.end(j),
                                     tl.masked(j), lim, lo, tl.sinks, h);
   uint32_t pk[16];
-  TileT::weights(x, c, mneg, pk, lsum);
-  TileT::template scores<1 - S>(smem, kbase_lane, qf, sacc);  // tile j+1
-  TileT::template values<S>(smem, vbase_lane, pk, oacc);
-  ld.template store_k<S>(smem);
-  ld.template store_v<1 - S>(smem);
+  TileT::weights(sacc[S], c, mneg, pk, lsum);
+  // Tile j+1's scores go to the other accumulator pair, so tile j's stay in place.
+  TileT::template scores<1 - S>(smem, kread, qf, sacc[1 - S]);
+  TileT::template values<S>(smem, vread, pk, oacc);
+  wait_tile_loads();
   __syncthreads();
 }
 
@@ -432,33 +400,46 @@ void attn_mfma_kernel(MfmaParams a) {
   float mref = kNegInf;  // reference maximum, base-2 units
   float lsum = 0.f;      // this lane's half of the row sum
   const float c = a.c_abs;
-  const int kbase_lane = ql * Geo::K_STRIDE + h * 16;
-  const int vbase_lane = ql * Geo::V_STRIDE + h * 16;
+  // Per-lane LDS byte offsets of the fragment reads inside a stage: K row ql,
+  // chunk 2s + h of k-step s; and, per 32-column tile dt of V^T, the
+  // transposing-read pointer of this lane (row 4(lane/32) + (lane%16)/4 of a
+  // 16-key step, 8 bytes at column 32 dt + 16 ((lane/16)%2) + 4 (lane%4)).
+  int kread[KSTEPS];
+#pragma unroll
+  for (int s = 0; s < KSTEPS; ++s) kread[s] = ql * Geo::ROW + ((2 * s + h) ^ Geo::swz_k(ql)) * 16;
+  int vread[DT];
+  {
+    const int j16 = lane & 15, grp = lane >> 4;
+    const int vr = 4 * (grp >> 1) + (j16 >> 2);
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+      const int d_off = 32 * dt + 16 * (grp & 1) + 4 * (j16 & 3);
+      vread[dt] = vr * Geo::ROW + (((d_off >> 3) ^ Geo::swz_v(vr)) * 16) + 2 * (d_off & 7);
+    }
+  }
 
   // Prologue: K and V of tile 0 into stage 0, K of tile 1 into K stage 1, then
   // tile 0's scores; the second barrier orders those K reads before stage 0 is
   // rewritten by the first pipelined step.
   Loader<D, NW> ld;
   ld.init();
-  floatx16 sacc[2];
+  floatx16 sacc[2][2];  // S^T of the current and the next tile
   if (ntiles > 0) {
-    ld.load_k(kh, tl.base(0), tl.end(0));
-    ld.load_v(vh, tl.base(0), tl.end(0));
-    ld.template store_k<0>(smem);
-    ld.template store_v<0>(smem);
-    ld.load_k(kh, tl.base(1), tl.end(1));
-    ld.template store_k<1>(smem);
+    ld.template load_k<0>(smem, kh, tl.base(0), tl.end(0));
+    ld.template load_v<0>(smem, vh, tl.base(0), tl.end(0));
+    ld.template load_k<1>(smem, kh, tl.base(1), tl.end(1));
   }
+  wait_tile_loads();
   __syncthreads();
-  if (ntiles > 0) TileT::template scores<0>(smem, kbase_lane, qf, sacc);
+  if (ntiles > 0) TileT::template scores<0>(smem, kread, qf, sacc[0]);
   __syncthreads();
 
   for (int j = 0; j < ntiles; j += 2) {
-    pipelined_step<D, NW, NEG, 0>(smem, ld, kh, vh, tl, j, lim, lo, h, kbase_lane, vbase_lane,
-                                  qf, sacc, oacc, lsum, mref, c);
+    pipelined_step<D, NW, NEG, 0>(smem, ld, kh, vh, tl, j, lim, lo, h, kread, vread, qf, sacc,
+                                  oacc, lsum, mref, c);
     if (j + 1 < ntiles)
-      pipelined_step<D, NW, NEG, 1>(smem, ld, kh, vh, tl, j + 1, lim, lo, h, kbase_lane,
-                                    vbase_lane, qf, sacc, oacc, lsum, mref, c);
+      pipelined_step<D, NW, NEG, 1>(smem, ld, kh, vh, tl, j + 1, lim, lo, h, kread, vread, qf,
+                                    sacc, oacc, lsum, mref, c);
   }
 
   // Row sum over both lane halves.
