@@ -45,6 +45,8 @@ def parse():
     ap.add_argument("--config", default="gqa_decode_b8_h32x8_kv4096_d128",
                     help="workload name (see paper_2609_12330_amd/workloads.py)")
     ap.add_argument("--seed", type=int, default=None)
+    ap.add_argument("--partition-size", type=int, default=None,
+                    help="keys per split-KV partition (default: the workload's, else the library's)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="CPU work budget of the oracle baseline (0 disables it)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -147,7 +149,8 @@ def main():
 
     W, S = cfg.window, cfg.sinks
     if decode:
-        T = ef.splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, cfg.partition_size, W, S)
+        T_req = cfg.partition_size if args.partition_size is None else args.partition_size
+        T = ef.splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, T_req, W, S)
         nbytes = ef.splitkv_workspace_size(B, Hq, Hkv, Sq, Skv, D, T, W, S)
         ws = ef.make_workspace(sets[0][0], sets[0][1], T, W, S)
         P = ef.splitkv_partitions(Sq, Skv, T, W, S)

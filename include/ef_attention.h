@@ -104,7 +104,7 @@ ef_status ef_attention_fwd_local(const void* q, const void* k, const void* v, fl
 /*
  * Partition size, in keys, that ef_attention_splitkv uses for these sizes:
  * `partition_size` itself when it is positive, else the library's choice
- * (a multiple of 64 that spreads the B*Hkv*P workgroups over the chip).
+ * (the candidate ef_attention_splitkv_modeled_us rates fastest).
  * Returns 0 when the arguments are invalid.
  */
 int ef_attention_splitkv_partition_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
@@ -215,6 +215,39 @@ ef_status ef_attention_splitkv_partials(const void* q, const void* k, const void
  */
 ef_status ef_attention_combine(const float* m, const float* l, const float* acc, float* o,
                                int rows, int num_partitions, int D, void* stream);
+
+/*
+ * Modelled duration in microseconds of one split-KV call with
+ * `partition_size` keys per partition (window = sinks = 0 for the causal or
+ * full entry point; a local window otherwise). The model is the roofline rule
+ * of section 6.3 (over legal schedules, minimise the largest work/throughput
+ * ratio over resources): the larger of the HBM time (K/V, q, o and the partial
+ * states written and read) and one workgroup's streaming time times the rounds
+ * of workgroups the chip holds, plus the combine, with rates measured on
+ * MI355X. With partition_size = 0 the split-KV entry points take the
+ * candidate (64, 128, 192, 256, 384, ... keys) this model rates fastest.
+ * Returns a negative value for invalid arguments.
+ */
+double ef_attention_splitkv_modeled_us(int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                       int window, int sinks, int partition_size);
+
+/*
+ * Measures the best partition size for these inputs on this device: the six
+ * candidates the model rates fastest (among those whose workspace fits in
+ * workspace_bytes) are timed by successive halving (section 6.3: every
+ * remaining candidate runs, the faster half stays, the repetitions double)
+ * and the winner is written to *partition_size. window = 0 selects the
+ * full/causal path (causal as given; sinks must be 0), window > 0 the local
+ * path. Runs the split-KV call many times on `stream` (o and the workspace
+ * are overwritten), waits for it with HIP events, and so cannot be captured
+ * in a graph. Errors as for the split-KV entry points; EF_ERR_NULL_POINTER
+ * when partition_size is NULL.
+ */
+ef_status ef_attention_splitkv_tune(const void* q, const void* k, const void* v, float* o,
+                                    int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                    float scale, int causal, int window, int sinks,
+                                    void* workspace, size_t workspace_bytes, void* stream,
+                                    int* partition_size);
 
 #ifdef __cplusplus
 }

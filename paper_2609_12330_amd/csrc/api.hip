@@ -1,8 +1,10 @@
 // Host side of the C ABI declared in include/ef_attention.h: argument
 // validation (synchronous, before anything is enqueued), kernel selection,
 // grid and workspace arithmetic.
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
+#include <vector>
 
 #include "ef_attention.h"
 #include "ef_device.hpp"
@@ -12,7 +14,6 @@ namespace {
 
 constexpr int kTileKeys = 64;        // key tile of the kernels; partitions are multiples of it
 constexpr int kDecodeMaxRows = 8;    // the VALU split producer serves G*Sq <= 8
-constexpr int kTargetBlocks = 1024;  // split producer workgroups the heuristic aims for
 constexpr int kMaxGridYZ = 65535;
 
 struct Shape {
@@ -69,18 +70,89 @@ ef::KeyRuns key_runs(int Sq, int Skv, int window, int sinks) {
   return r;
 }
 
-// Keys per partition of a key axis of `keys` keys (the visible runs' length).
+// Roofline model of one split-KV call with T keys per partition (section 6.3:
+// over the legal schedules, minimise the largest work/throughput ratio over
+// the modelled resources). Resources: HBM (K/V, q, o and the partial states
+// written and read back) and the streaming time of one workgroup (T keys of K
+// and V at a per-wave rate, times the rounds of workgroups the chip holds);
+// the combine follows (inside the producer for small P, else a second
+// kernel). The rates are measured on MI355X: 6.5 TB/s streaming reads (the
+// VALU decode producer), 5.0 TB/s for the MFMA producer, 8 and 5 GB/s per
+// wave, 2048 resident waves, about 3 us of fixed cost per workgroup round, 4
+// us for the combine inside the producer and 5 us plus its reads for the
+// combine kernel.
+constexpr double kHbmValuBytesPerUs = 6.5e6;
+constexpr double kHbmMfmaBytesPerUs = 5.0e6;
+constexpr double kWaveValuBytesPerUs = 8.0e3;
+constexpr double kWaveMfmaBytesPerUs = 5.0e3;
+constexpr double kResidentWaves = 2048.0;
+constexpr double kRoundUs = 3.0;
+constexpr double kFusedCombineUs = 4.0;
+constexpr double kCombineLaunchUs = 5.0;
+
+double split_model_us(const Shape& s, int keys, int T) {
+  const int G = s.Hq / s.Hkv;
+  const int R = G * s.Sq;
+  const double P = std::ceil((double)keys / T);
+  const bool valu = R <= kDecodeMaxRows;
+  double nw, wg_per_part;
+  if (valu) {
+    const int rmax = R <= 1 ? 1 : R <= 2 ? 2 : R <= 4 ? 4 : 8;
+    nw = (rmax == 1 || rmax == 4) ? 1 : 2;  // waves per workgroup of the VALU producer
+    wg_per_part = 1;
+  } else {
+    const int bm = ef::mfma_rows_per_block(R);
+    nw = bm / 32;
+    wg_per_part = std::ceil((double)R / bm);
+  }
+  const double kv_heads = (double)s.B * s.Hkv;
+  const double rows = (double)s.B * s.Hq * s.Sq;
+  const double kv_bytes = kv_heads * keys * s.D * 4.0;
+  const double io_bytes = rows * s.D * 6.0;
+  const double state_bytes = rows * P * (s.D + 2) * 4.0;
+  const double r_hbm = (kv_bytes + io_bytes + 2.0 * state_bytes) /
+                       (valu ? kHbmValuBytesPerUs : kHbmMfmaBytesPerUs);
+  const double waves = kv_heads * P * wg_per_part * nw;
+  const double rounds = std::ceil(waves / kResidentWaves);
+  const double wave_rate = valu ? kWaveValuBytesPerUs : kWaveMfmaBytesPerUs;
+  const double r_wg = rounds * ((double)T * s.D * 4.0 / (wave_rate * nw) + kRoundUs);
+  const bool fused = valu && P <= ef::kFusedMaxP;
+  const double combine = fused ? kFusedCombineUs : state_bytes / kHbmValuBytesPerUs + kCombineLaunchUs;
+  return std::max(r_hbm, r_wg) + combine;
+}
+
+// Candidate partition sizes for a key axis of `keys` keys: 64, 128, 192, 256,
+// 384, 512, ... (powers of two times 64 and 1.5 times them), up to one
+// partition holding every key; at most 65535 partitions.
+std::vector<int> partition_candidates(int keys) {
+  std::vector<int> out;
+  const long long top = ((long long)std::max(keys, 1) + kTileKeys - 1) / kTileKeys * kTileKeys;
+  for (long long t = kTileKeys; t < top; t *= 2) {
+    if ((keys + t - 1) / t <= kMaxGridYZ) out.push_back((int)t);
+    const long long t3 = t * 3 / 2;
+    if (t3 % kTileKeys == 0 && t3 < top && (keys + t3 - 1) / t3 <= kMaxGridYZ) out.push_back((int)t3);
+  }
+  out.push_back((int)top);
+  std::sort(out.begin(), out.end());
+  out.erase(std::unique(out.begin(), out.end()), out.end());
+  return out;
+}
+
+// Keys per partition of a key axis of `keys` keys (the visible runs' length):
+// the caller's choice, else the candidate the model rates fastest.
 int resolve_partition(const Shape& s, int keys, int partition_size) {
   if (partition_size > 0) return partition_size;
   if (keys <= 0) return kTileKeys;
-  const long long kv_heads = (long long)s.B * s.Hkv;
-  long long parts = (kTargetBlocks + kv_heads - 1) / kv_heads;
-  if (parts < 1) parts = 1;
-  long long t = (keys + parts - 1) / parts;
-  t = (t + kTileKeys - 1) / kTileKeys * kTileKeys;
-  if (t < 256) t = 256;  // keep the stored state small against the K/V bytes read
-  if (t > keys) t = (keys + kTileKeys - 1) / kTileKeys * kTileKeys;
-  return (int)t;
+  int best = kTileKeys;
+  double best_us = 1e300;
+  for (int t : partition_candidates(keys)) {
+    const double us = split_model_us(s, keys, t);
+    if (us < best_us) {
+      best_us = us;
+      best = t;
+    }
+  }
+  return best;
 }
 
 ef_status check_mask(int window, int sinks) {
@@ -386,6 +458,87 @@ ef_status ef_attention_combine(const float* m, const float* l, const float* acc,
   c.P = num_partitions;
   c.D = D;
   return from_hip(ef::launch_combine(c, static_cast<hipStream_t>(stream)));
+}
+
+double ef_attention_splitkv_modeled_us(int B, int Hq, int Hkv, int Sq, int Skv, int D, int window,
+                                        int sinks, int partition_size) {
+  const Shape s{B, Hq, Hkv, Sq, Skv, D};
+  if (check_shape(s) != EF_OK || window < 0 || sinks < 0) return -1.0;
+  if (partition_size <= 0 || partition_size % kTileKeys != 0) return -1.0;
+  const ef::KeyRuns runs = key_runs(Sq, Skv, window, sinks);
+  if (s.rows() == 0 || runs.lv == 0) return 0.0;
+  return split_model_us(s, runs.lv, partition_size);
+}
+
+ef_status ef_attention_splitkv_tune(const void* q, const void* k, const void* v, float* o, int B,
+                                    int Hq, int Hkv, int Sq, int Skv, int D, float scale,
+                                    int causal, int window, int sinks, void* workspace,
+                                    size_t workspace_bytes, void* stream, int* partition_size) {
+  if (partition_size == nullptr) return EF_ERR_NULL_POINTER;
+  const Shape s{B, Hq, Hkv, Sq, Skv, D};
+  ef_status st = check_shape(s);
+  if (st != EF_OK) return st;
+  if (window < 0 || sinks < 0 || (window == 0 && sinks != 0)) return EF_ERR_INVALID_MASK;
+  st = check_io(s, q, k, v, o, scale);
+  if (st != EF_OK) return st;
+  const bool local = window > 0;
+  const ef::KeyRuns runs = key_runs(Sq, Skv, window, sinks);
+  if (s.rows() == 0 || runs.lv == 0) {
+    *partition_size = resolve_partition(s, runs.lv, 0);
+    return EF_OK;
+  }
+  // Candidates the model rates best, whose workspace fits.
+  std::vector<std::pair<double, int>> ranked;
+  for (int t : partition_candidates(runs.lv)) {
+    if (workspace_size_impl(s, runs, t) <= workspace_bytes)
+      ranked.push_back({split_model_us(s, runs.lv, t), t});
+  }
+  if (ranked.empty()) return EF_ERR_WORKSPACE_TOO_SMALL;
+  std::sort(ranked.begin(), ranked.end());
+  constexpr size_t kTried = 6;
+  if (ranked.size() > kTried) ranked.resize(kTried);
+  std::vector<int> cands;
+  for (const auto& r : ranked) cands.push_back(r.second);
+
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) {
+    if (e0) (void)hipEventDestroy(e0);
+    return EF_ERR_HIP;
+  }
+  auto call = [&](int t) {
+    return splitkv_impl(s, q, k, v, o, scale, local ? 1 : causal, runs, t, workspace,
+                        workspace_bytes, stream);
+  };
+  // Successive halving (section 6.3, progressive tuning): time every
+  // remaining candidate, keep the faster half, double the repetitions.
+  int reps = 2;
+  while (cands.size() > 1 && st == EF_OK) {
+    std::vector<std::pair<float, int>> timed;
+    for (int t : cands) {
+      st = call(t);  // warm-up
+      if (st != EF_OK) break;
+      if (hipEventRecord(e0, hs) != hipSuccess) { st = EF_ERR_HIP; break; }
+      for (int r = 0; r < reps && st == EF_OK; ++r) st = call(t);
+      if (st != EF_OK) break;
+      float ms = 0.f;
+      if (hipEventRecord(e1, hs) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+          hipEventElapsedTime(&ms, e0, e1) != hipSuccess) {
+        st = EF_ERR_HIP;
+        break;
+      }
+      timed.push_back({ms, t});
+    }
+    if (st != EF_OK) break;
+    std::stable_sort(timed.begin(), timed.end());
+    cands.clear();
+    for (size_t i = 0; i < (timed.size() + 1) / 2; ++i) cands.push_back(timed[i].second);
+    reps *= 2;
+  }
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (st == EF_OK) *partition_size = cands.front();
+  return st;
 }
 
 }  // extern "C"

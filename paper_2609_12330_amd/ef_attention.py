@@ -50,6 +50,9 @@ SIGNATURES = {
                                         _i, _vp, _sz, _vp]),
     "ef_attention_splitkv_local_partition_size": (_i, [_i, _i, _i, _i, _i, _i, _i, _i, _i]),
     "ef_attention_splitkv_local_workspace_size": (_sz, [_i, _i, _i, _i, _i, _i, _i, _i, _i]),
+    "ef_attention_splitkv_modeled_us": (ctypes.c_double, [_i, _i, _i, _i, _i, _i, _i, _i, _i]),
+    "ef_attention_splitkv_tune": (_i, [_vp, _vp, _vp, _fp, _i, _i, _i, _i, _i, _i, _f, _i, _i, _i,
+                                       _vp, _sz, _vp, ctypes.POINTER(ctypes.c_int)]),
 }
 
 
@@ -146,6 +149,20 @@ def ef_attention_splitkv_local_workspace_size(B, Hq, Hkv, Sq, Skv, D, window, si
                                               partition_size) -> int:
     return _lib().ef_attention_splitkv_local_workspace_size(B, Hq, Hkv, Sq, Skv, D, window,
                                                             sinks, partition_size)
+
+
+def ef_attention_splitkv_modeled_us(B, Hq, Hkv, Sq, Skv, D, window, sinks, partition_size) -> float:
+    return _lib().ef_attention_splitkv_modeled_us(B, Hq, Hkv, Sq, Skv, D, window, sinks,
+                                                  partition_size)
+
+
+def ef_attention_splitkv_tune(q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale, causal, window, sinks,
+                              workspace, workspace_bytes, stream, partition_size) -> int:
+    """`partition_size` is a ctypes.c_int (passed by reference) or None."""
+    ptr = ctypes.byref(partition_size) if partition_size is not None else None
+    return _lib().ef_attention_splitkv_tune(q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale,
+                                            int(causal), window, sinks, workspace,
+                                            workspace_bytes, stream, ptr)
 
 
 # ---------------------------------------------------------------------------
@@ -366,3 +383,26 @@ def combine(m, l, acc, out=None, stream=None):
                               _stream_handle(stream))
     _check(st, "ef_attention_combine")
     return o
+
+
+def tune_partition_size(q, k, v, scale: Optional[float] = None, causal: bool = False,
+                        window: int = 0, sinks: int = 0, workspace=None, stream=None) -> int:
+    """Measured best split-KV partition size for these inputs (ef_attention_splitkv_tune).
+    Without a workspace, one large enough for every candidate of at least 64 keys is made."""
+    torch = _torch()
+    B, Hq, Hkv, Sq, Skv, D = _check_qkv(q, k, v)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    local = _local(causal, window, sinks)
+    if workspace is None:
+        workspace = make_workspace(q, k, 64, window, sinks)
+    _check_workspace(workspace, q)
+    o = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+    t = ctypes.c_int(0)
+    st = ef_attention_splitkv_tune(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B, Hq,
+                                   Hkv, Sq, Skv, D, float(scale), causal, window if local else 0,
+                                   sinks if local else 0, workspace.data_ptr(),
+                                   workspace.numel() * workspace.element_size(),
+                                   _stream_handle(stream), t)
+    _check(st, "ef_attention_splitkv_tune")
+    return int(t.value)

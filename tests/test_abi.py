@@ -37,7 +37,8 @@ def test_header_declares_the_entry_points():
               "ef_attention_splitkv_workspace_size", "ef_attention_splitkv_partition_size",
               "ef_attention_fwd_local", "ef_attention_splitkv_local",
               "ef_attention_splitkv_local_workspace_size",
-              "ef_attention_splitkv_local_partition_size", "ef_status_string", "ef_abi_version"):
+              "ef_attention_splitkv_local_partition_size", "ef_attention_splitkv_modeled_us",
+              "ef_attention_splitkv_tune", "ef_status_string", "ef_abi_version"):
         assert n in names
     assert set(names) == set(ef.SIGNATURES), "binding signatures must cover the header exactly"
 
@@ -230,14 +231,57 @@ def test_local_workspace_and_partition_arithmetic():
         2, 8, 2, 1, 1000, 128, 0)
     assert ps(2, 8, 2, 1, 1000, 128, 5000, 0, 0) == ef.ef_attention_splitkv_partition_size(
         2, 8, 2, 1, 1000, 128, 0)
-    # the library's partition choice splits the visible runs (4160 keys), not the whole
-    # key axis: 128 partitions per kv head would be wanted, the 256-key floor gives 17
-    assert ps(1, 32, 8, 1, 131072, 128, 4096, 4, 0) == 256
+    # the library's partition choice splits the visible runs (4160 keys), not the whole key axis
+    t = ps(1, 32, 8, 1, 131072, 128, 4096, 4, 0)
+    assert t % 64 == 0 and t <= 4160
     assert ps(1, 32, 8, 1, 131072, 128, 131072, 4, 0) == 1024 == ef.ef_attention_splitkv_partition_size(
         1, 32, 8, 1, 131072, 128, 0)
     assert ps(1, 4, 2, 1, 1000, 128, 0, 0, 0) == 0
     assert ws(1, 4, 2, 1, 1000, 128, 64, -1, 0) == 0
     assert ps(1, 4, 2, 1, 1000, 128, 64, 0, 100) == 0
+
+
+@needs_lib
+def test_roofline_partition_choice():
+    """partition_size = 0 takes the candidate the roofline model rates fastest; on MI355X the
+    model's picks are the measured best of {256, ..., 4096} for these three decodes."""
+    ps = ef.ef_attention_splitkv_partition_size
+    model = ef.ef_attention_splitkv_modeled_us
+    assert ps(8, 32, 8, 1, 4096, 128, 0) == 256        # GQA decode: 16 partitions, fused combine
+    assert ps(1, 32, 8, 1, 131072, 128, 0) == 1024     # 131072-key decode
+    assert ps(16, 64, 8, 8, 8192, 128, 0) == 2048      # chunked decode (MFMA producer)
+    for shape in [(8, 32, 8, 1, 4096, 128), (1, 32, 8, 1, 131072, 128), (16, 64, 8, 8, 8192, 128),
+                  (2, 8, 2, 3, 900, 128), (1, 4, 4, 1, 70, 64)]:
+        t = ps(*shape, 0)
+        assert t > 0 and t % 64 == 0
+        best = model(*shape, 0, 0, t)
+        assert best > 0
+        for cand in (64, 128, 192, 256, 384, 512, 768, 1024, 2048, 4096):
+            if cand <= -(-shape[4] // 64) * 64:
+                assert model(*shape, 0, 0, cand) >= best - 1e-9, (shape, cand)
+    # the model: more partitions cost combine traffic, fewer cost per-workgroup streaming time
+    assert model(1, 32, 8, 1, 131072, 128, 0, 0, 64) > model(1, 32, 8, 1, 131072, 128, 0, 0, 1024)
+    assert model(1, 32, 8, 1, 131072, 128, 0, 0, 16384) > model(1, 32, 8, 1, 131072, 128, 0, 0, 1024)
+    # local attention: the model sees only the visible runs
+    assert ef.ef_attention_splitkv_local_partition_size(1, 32, 8, 1, 131072, 128, 4096, 4, 0) <= 4160
+    assert model(1, 4, 2, 1, 1000, 128, 0, 0, 100) < 0
+    assert model(1, 4, 2, 1, 1000, 96, 0, 0, 64) < 0
+    assert model(0, 4, 2, 1, 1000, 128, 0, 0, 64) == 0
+
+
+@needs_lib
+def test_tune_validation():
+    import ctypes as C
+    t = C.c_int(0)
+    tune = ef.ef_attention_splitkv_tune
+    args = (A, A, A, A, 1, 4, 2, 1, 1000, 128, 0.1, 0)
+    assert tune(*args, 0, 0, A, 1 << 30, None, None) == 1
+    assert tune(*args, -1, 0, A, 1 << 30, None, t) == 10
+    assert tune(*args, 0, 3, A, 1 << 30, None, t) == 10
+    assert tune(A, A, A, A, 1, 4, 2, 1, 1000, 96, 0.1, 0, 0, 0, A, 1 << 30, None, t) == 4
+    assert tune(*args, 0, 0, A, 16, None, t) == 7  # no candidate's workspace fits
+    assert tune(A, A, A, A, 0, 4, 2, 1, 1000, 128, 0.1, 0, 0, 0, A, 0, None, t) == 0
+    assert t.value > 0
 
 
 def test_binding_fails_loudly_without_library(monkeypatch):
