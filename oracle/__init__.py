@@ -19,3 +19,4 @@ from .attention import (  # noqa: F401
     rolling_update,
     splitkv_partials_ref,
 )
+from .differential import diff_attention_ref, mixing_weight, rms_norm_rows  # noqa: F401

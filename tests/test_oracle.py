@@ -609,3 +609,157 @@ def test_mutant_sinks_ignored(monkeypatch):
     monkeypatch.setattr(oa, "visible", lambda Sq, Skv, c, w=0, s=0: real(Sq, Skv, c, w, 0))
     with pytest.raises(AssertionError):
         test_golden_local_cases()
+
+
+# ---------------------------------------------------------------------------
+# Differential attention (section 7.3): two branches sharing v, their weighted
+# difference normalised per head.
+# ---------------------------------------------------------------------------
+
+import oracle.differential as od  # noqa: E402
+
+_DIFF_CONSTS = {"ln3": math.log(3.0), "ln2": math.log(2.0), "0.48*sqrt2": 0.48 * math.sqrt(2.0),
+                "1.28*sqrt2": 1.28 * math.sqrt(2.0)}
+
+
+def _dv(x):
+    if isinstance(x, list):
+        return [_dv(e) for e in x]
+    return _DIFF_CONSTS[x] if isinstance(x, str) else float(x)
+
+
+def _diff_case(c, fn=None):
+    fn = fn or oracle.diff_attention_ref
+    a = {k: np.array(_dv(c[k])) for k in ("q1", "q2", "k1", "k2", "v", "lq1", "lk1", "lq2",
+                                          "lk2", "gamma")}
+    return fn(a["q1"], a["q2"], a["k1"], a["k2"], a["v"], a["lq1"], a["lk1"], a["lq2"], a["lk2"],
+              a["gamma"], c["lambda_init"], c["eps"], c["scale"], c["causal"])
+
+
+def _diff_golden_ok(fn=None):
+    for c in json.load(open(GOLDEN))["differential"]:
+        if not np.allclose(_diff_case(c, fn), np.array(_dv(c["o"])), rtol=0, atol=1e-12):
+            return False
+    return True
+
+
+def test_diff_golden_cases():
+    assert _diff_golden_ok()
+
+
+def _diff_inputs(B, Hq, Hkv, Sq, Skv, D, seed):
+    r = np.random.default_rng(seed)
+    q1, q2 = r.standard_normal((2, B, Hq, Sq, D))
+    k1, k2 = r.standard_normal((2, B, Hkv, Skv, D))
+    v = r.standard_normal((B, Hkv, Skv, D))
+    lam = r.standard_normal((4, D)) * 0.1
+    gamma = 1.0 + 0.1 * r.standard_normal(D)
+    return q1, q2, k1, k2, v, lam, gamma
+
+
+def _diff_call(inp, lambda_init=0.2, eps=0.0, scale=0.3, causal=True, fn=None):
+    q1, q2, k1, k2, v, lam, gamma = inp
+    fn = fn or oracle.diff_attention_ref
+    return fn(q1, q2, k1, k2, v, lam[0], lam[1], lam[2], lam[3], gamma, lambda_init, eps, scale,
+              causal)
+
+
+def _diff_rms_ok(fn=None):
+    """gamma = 1, eps = 0: every output row has RMS |1 - lambda_init|."""
+    inp = list(_diff_inputs(2, 4, 2, 5, 9, 8, seed=61))
+    inp[6] = np.ones(8)
+    o = _diff_call(inp, lambda_init=0.3, fn=fn)
+    return np.allclose(np.sqrt(np.mean(o * o, axis=-1)), 0.7, atol=1e-12)
+
+
+def _diff_scale_invariance_ok(fn=None):
+    """eps = 0: scaling v by c > 0 leaves the output unchanged, c < 0 flips its sign."""
+    inp = _diff_inputs(1, 2, 1, 4, 7, 8, seed=62)
+    base = _diff_call(inp, fn=fn)
+    big = list(inp)
+    big[4] = inp[4] * 3.5
+    neg = list(inp)
+    neg[4] = -inp[4]
+    return (np.allclose(_diff_call(big, fn=fn), base, atol=1e-12)
+            and np.allclose(_diff_call(neg, fn=fn), -base, atol=1e-12))
+
+
+def _diff_cancel_ok(fn=None):
+    """Equal branches with lambda = 1 cancel: y = 0, so the output is 0 for eps > 0."""
+    q1, q2, k1, k2, v, lam, gamma = _diff_inputs(1, 2, 2, 3, 5, 4, seed=63)
+    z = np.zeros(4)
+    # exp(0) - exp(0) + lambda_init = lambda_init = 1
+    o = (fn or oracle.diff_attention_ref)(q1, q1, k1, k1, v, z, z, z, z, gamma, 1.0, 1e-6, 0.5,
+                                          False)
+    return np.abs(o).max() == 0.0
+
+
+def _diff_branch_ok(fn=None):
+    """lambda = 0 (lambda_init = -(e^a - e^b) makes the branches' weight vanish), eps = 0:
+    the output is branch 1's attention, RMS-normalised, times gamma and 1 - lambda_init,
+    with branch 1 taken from torch's SDPA (an independent library routine)."""
+    q1, q2, k1, k2, v, lam, gamma = _diff_inputs(1, 4, 2, 6, 11, 8, seed=64)
+    a = float(np.dot(lam[0], lam[1]))
+    b = float(np.dot(lam[2], lam[3]))
+    li = -(math.exp(a) - math.exp(b))
+    o = (fn or oracle.diff_attention_ref)(q1, q2, k1, k2, v, lam[0], lam[1], lam[2], lam[3], gamma,
+                                          li, 0.0, 0.4, True)
+    a1 = _sdpa64(q1, k1, v, 0.4, True)
+    want = (1.0 - li) * gamma * a1 / np.sqrt(np.mean(a1 * a1, axis=-1, keepdims=True))
+    return np.allclose(o, want, atol=1e-10)
+
+
+def test_diff_rms_of_rows():
+    assert _diff_rms_ok()
+
+
+def test_diff_scale_invariance():
+    assert _diff_scale_invariance_ok()
+
+
+def test_diff_equal_branches_cancel():
+    assert _diff_cancel_ok()
+
+
+def test_diff_single_branch_matches_sdpa():
+    assert _diff_branch_ok()
+
+
+def _diff_all_pins(fn):
+    return all(f(fn) for f in (_diff_golden_ok, _diff_rms_ok, _diff_scale_invariance_ok,
+                               _diff_cancel_ok, _diff_branch_ok))
+
+
+def test_diff_pins_pass_for_the_oracle():
+    assert _diff_all_pins(None)
+
+
+def _diff_mutant(kind):
+    def fn(q1, q2, k1, k2, v, lq1, lk1, lq2, lk2, gamma, lambda_init, eps, scale, causal=False):
+        a1 = oracle.attention_ref(q1, k1, v, scale, causal)
+        a2 = oracle.attention_ref(q2, k2, v, scale, causal)
+        lam = od.mixing_weight(lq1, lk1, lq2, lk2, lambda_init)
+        if kind == "lambda_sign":
+            y = a1 + lam * a2
+        else:
+            y = a1 - lam * a2
+        if kind == "lambda_plus":
+            lam2 = float(np.exp(np.dot(lq1, lk1)) + np.exp(np.dot(lq2, lk2)) + lambda_init)
+            y = a1 - lam2 * a2
+        if kind == "norm_axis":
+            ms = np.mean(y * y, axis=-2, keepdims=True)
+            out = np.asarray(gamma) * y / np.sqrt(ms + eps)
+        else:
+            out = od.rms_norm_rows(y, gamma, eps)
+        if kind == "no_init_factor":
+            return out
+        if kind == "branches_swapped":
+            out = od.rms_norm_rows(a2 - lam * a1, gamma, eps)
+        return (1.0 - lambda_init) * out
+    return fn
+
+
+@pytest.mark.parametrize("kind", ["lambda_sign", "lambda_plus", "norm_axis", "no_init_factor",
+                                  "branches_swapped"])
+def test_diff_mutants_are_caught(kind):
+    assert not _diff_all_pins(_diff_mutant(kind)), f"mutant {kind} passes every pin"
