@@ -37,10 +37,14 @@ def mixing_weight(lq1, lk1, lq2, lk2, lambda_init: float) -> float:
 
 
 def rms_norm_rows(y, gamma, eps: float) -> np.ndarray:
-    """gamma * y / sqrt(mean(y^2) + eps) over the last axis."""
+    """gamma * y / sqrt(mean(y^2) + eps) over the last axis.
+
+    A row whose mean(y^2) + eps is 0 (y = 0 with eps = 0) has no defined
+    normalisation; it is read as the zero row, the limit of the eps > 0 case."""
     y = np.asarray(y, dtype=np.float64)
-    ms = np.mean(y * y, axis=-1, keepdims=True)
-    return np.asarray(gamma, np.float64) * y / np.sqrt(ms + eps)
+    den = np.sqrt(np.mean(y * y, axis=-1, keepdims=True) + eps)
+    safe = np.where(den > 0.0, den, 1.0)
+    return np.where(den > 0.0, np.asarray(gamma, np.float64) * y / safe, 0.0)
 
 
 def diff_attention_ref(q1, q2, k1, k2, v, lq1, lk1, lq2, lk2, gamma, lambda_init: float,

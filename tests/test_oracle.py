@@ -694,6 +694,20 @@ def _diff_cancel_ok(fn=None):
     return np.abs(o).max() == 0.0
 
 
+def _diff_zero_rows_ok(fn=None):
+    """eps = 0 and y = 0 (equal branches with lambda = 1, or causal rows that see no key):
+    the normalisation is read as giving the zero row, never NaN."""
+    q1, q2, k1, k2, v, lam, gamma = _diff_inputs(1, 2, 1, 6, 3, 4, seed=65)
+    z = np.zeros(4)
+    fn = fn or oracle.diff_attention_ref
+    same = fn(q1, q1, k1, k1, v, z, z, z, z, gamma, 1.0, 0.0, 0.5, False)
+    # Causal, Sq = 6 > Skv = 3: the first three query rows see no key.
+    masked = fn(q1, q2, k1, k2, v, lam[0], lam[1], lam[2], lam[3], gamma, 0.2, 0.0, 0.5, True)
+    return (np.array_equal(same, np.zeros_like(same))
+            and np.array_equal(masked[:, :, :3], np.zeros_like(masked[:, :, :3]))
+            and bool(np.all(np.isfinite(masked))) and np.abs(masked[:, :, 3:]).min() > 0.0)
+
+
 def _diff_branch_ok(fn=None):
     """lambda = 0 (lambda_init = -(e^a - e^b) makes the branches' weight vanish), eps = 0:
     the output is branch 1's attention, RMS-normalised, times gamma and 1 - lambda_init,
@@ -723,6 +737,10 @@ def test_diff_equal_branches_cancel():
 
 def test_diff_single_branch_matches_sdpa():
     assert _diff_branch_ok()
+
+
+def test_diff_zero_rows():
+    assert _diff_zero_rows_ok()
 
 
 def _diff_all_pins(fn):
