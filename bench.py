@@ -14,7 +14,8 @@ cost stays out of the figure (the paper times under CUDA Graphs).
 Prints one JSON line. `--config` selects another workload (the causal prefill
 is reported in TFLOP/s through ef_attention_fwd; the local-attention workloads
 run through the *_local entry points and count only the keys their window and
-sinks let some query see).
+sinks let some query see; the differential-attention layer runs through
+ef_diff_attention and counts the flops of both branches).
 """
 
 from __future__ import annotations
@@ -66,10 +67,10 @@ def load_traffic(kernel_key, src_hash, units_per_launch):
     return float(t["hbm_bytes_per_launch"])
 
 
-def cpu_baseline(cfg, q, k, v, budget_s, unit_fn):
-    """Time the fp64 oracle as it stands on this host over repeated passes of the workload."""
-    import numpy as np
-
+def cpu_baseline(cfg, inputs, budget_s, unit_fn):
+    """Time the fp64 oracle as it stands on this host over repeated passes of a bounded
+    sample of the workload: batch row 0 (head 0 of batch row 0 for the differential layer,
+    whose batch has one row)."""
     import oracle
     from paper_2609_12330_amd import workloads as wl
 
@@ -81,12 +82,28 @@ def cpu_baseline(cfg, q, k, v, budget_s, unit_fn):
         threads = max((i.get("num_threads") or 0) for i in info) if info else None
     except Exception:
         pass
-    Q, K, V = wl.to_f64(q), wl.to_f64(k), wl.to_f64(v)
-    # Bound the sample: whole kv-head groups of the workload, enough for ~budget_s of work.
-    B = cfg.B
-    def run():
-        oracle.attention_ref(Q[:1], K[:1], V[:1], cfg.scale, cfg.causal, window=cfg.window,
-                             sinks=cfg.sinks)
+    if cfg.diff:
+        q1, q2, k1, k2, v, lam, gamma = inputs
+        h = slice(0, 1)
+        Q1, Q2 = wl.to_f64(q1[:1, h]), wl.to_f64(q2[:1, h])
+        K1, K2, V = wl.to_f64(k1[:1, h]), wl.to_f64(k2[:1, h]), wl.to_f64(v[:1, h])
+        L = [wl.to_f64(t) for t in lam]
+        Gm = wl.to_f64(gamma)
+        frac = 1.0 / (cfg.B * cfg.Hq)
+        what = "head 0 of batch row 0"
+
+        def run():
+            oracle.diff_attention_ref(Q1, Q2, K1, K2, V, *L, Gm, wl.DIFF_LAMBDA_INIT, wl.DIFF_EPS,
+                                      cfg.scale, cfg.causal)
+    else:
+        q, k, v = inputs
+        Q, K, V = wl.to_f64(q[:1]), wl.to_f64(k[:1]), wl.to_f64(v[:1])
+        frac = 1.0 / cfg.B
+        what = "batch row 0"
+
+        def run():
+            oracle.attention_ref(Q, K, V, cfg.scale, cfg.causal, window=cfg.window,
+                                 sinks=cfg.sinks)
 
     run()  # warm caches and pools
     t0 = time.perf_counter()
@@ -97,12 +114,12 @@ def cpu_baseline(cfg, q, k, v, budget_s, unit_fn):
     for _ in range(reps):
         run()
     dt = time.perf_counter() - t0
-    value = unit_fn(reps / B) / dt  # the work of `reps` batch rows of the workload per second
+    value = unit_fn(reps * frac) / dt  # the work of `reps` samples of the workload per second
     return {
         "value": round(value, 4),
         "cores": threads or os.cpu_count(),
         "kind": "oracle",
-        "sample": f"{reps} passes of batch row 0 of the workload (Hq={cfg.Hq}, Hkv={cfg.Hkv}, "
+        "sample": f"{reps} passes of {what} of the workload (Hq={cfg.Hq}, Hkv={cfg.Hkv}, "
                   f"Sq={cfg.Sq}, Skv={cfg.Skv}, D={cfg.D}) through the fp64 numpy oracle, "
                   f"inputs widened to fp64 once outside the timing; {dt:.1f} s",
     }
@@ -129,20 +146,34 @@ def main():
     cfg = wl.CONFIG_BY_NAME[args.config]
     seed = args.seed if args.seed is not None else wl.DEFAULT_SEED[cfg.name]
     dev = torch.device("cuda:0")
-    decode = cfg.Sq * cfg.G <= 64 and cfg.Skv >= 1024 and not (cfg.Sq == cfg.Skv)
+    decode = (cfg.Sq * cfg.G <= 64 and cfg.Skv >= 1024 and not (cfg.Sq == cfg.Skv)
+              and not cfg.diff)
 
     # Buffer sets: the K/V of consecutive steps never share a 256 MB cache footprint.
     kv = cfg.kv_bytes()
     nbuf = 1 if kv == 0 else max(2, math.ceil(2.5 * MALL_BYTES / kv))
     nbuf = min(nbuf, 8)
-    q_cpu, k_cpu, v_cpu = wl.make_inputs(cfg, seed)
-    sets = []
-    for i in range(nbuf):
-        if i == 0:
-            q, k, v = q_cpu, k_cpu, v_cpu
-        else:
-            q, k, v = wl.make_inputs(cfg, seed + 1000 * i)
-        sets.append((q.to(dev), k.to(dev), v.to(dev)))
+    if cfg.diff:
+        # Three K/V-sized tensors per set (k1, k2, v).
+        nbuf = min(8, max(2, math.ceil(2.5 * MALL_BYTES / (3 * kv // 2))))
+        cpu_inputs = wl.make_diff_inputs(cfg.B, cfg.Hq, cfg.Hkv, cfg.Sq, cfg.Skv, cfg.D, seed)
+        diff_sets = []
+        for i in range(nbuf):
+            x = cpu_inputs if i == 0 else wl.make_diff_inputs(
+                cfg.B, cfg.Hq, cfg.Hkv, cfg.Sq, cfg.Skv, cfg.D, seed + 1000 * i)
+            q1, q2, k1, k2, v, lam, gamma = x
+            diff_sets.append([t.to(dev) for t in (q1, q2, k1, k2, v, *lam, gamma)])
+        sets = [(d[0], d[2], d[4]) for d in diff_sets]  # branch 1 q, k and the shared v
+    else:
+        q_cpu, k_cpu, v_cpu = wl.make_inputs(cfg, seed)
+        cpu_inputs = (q_cpu, k_cpu, v_cpu)
+        sets = []
+        for i in range(nbuf):
+            if i == 0:
+                q, k, v = q_cpu, k_cpu, v_cpu
+            else:
+                q, k, v = wl.make_inputs(cfg, seed + 1000 * i)
+            sets.append((q.to(dev), k.to(dev), v.to(dev)))
     o = torch.empty(cfg.B, cfg.Hq, cfg.Sq, cfg.D, dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream()
     B, Hq, Hkv, Sq, Skv, D = cfg.B, cfg.Hq, cfg.Hkv, cfg.Sq, cfg.Skv, cfg.D
@@ -212,6 +243,41 @@ def main():
         if single_call:
             def produce(i):  # noqa: F811  (one call: producer with the combine inside)
                 step(i)
+    elif cfg.diff:
+        T = ef.splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D,
+                                      0 if args.partition_size is None else args.partition_size)
+        P = ef.splitkv_partitions(Sq, Skv, T)
+        wsb = max(256, int(ef.ef_diff_attention_workspace_size(B, Hq, Hkv, Sq, Skv, D, T)))
+        ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+
+        def step(i, ev=None):
+            d = diff_sets[i % nbuf]
+            cur = torch.cuda.current_stream()
+            if ev is not None:
+                ev[0].record(cur)
+            st = ef.ef_diff_attention(*(t.data_ptr() for t in d[:5]), o.data_ptr(),
+                                      *(t.data_ptr() for t in d[5:]), wl.DIFF_LAMBDA_INIT,
+                                      wl.DIFF_EPS, B, Hq, Hkv, Sq, Skv, D, cfg.scale, cfg.causal,
+                                      T, ws.data_ptr(), wsb, cur.cuda_stream)
+            if ev is not None:
+                ev[1].record(cur)
+                ev[2].record(cur)
+            if st:
+                raise RuntimeError(f"library error {st}")
+
+        def produce(i):
+            """One branch's attention kernel alone, as ef_diff_attention launches it."""
+            q, k, v = sets[i % nbuf]
+            sh = torch.cuda.current_stream().cuda_stream
+            if P > 1:
+                st = ef.ef_attention_splitkv_partials(q.data_ptr(), k.data_ptr(), v.data_ptr(), B,
+                                                      Hq, Hkv, Sq, Skv, D, cfg.scale, cfg.causal,
+                                                      T, ws.data_ptr(), wsb, sh)
+            else:
+                st = ef.ef_attention_fwd(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(),
+                                         B, Hq, Hkv, Sq, Skv, D, cfg.scale, cfg.causal, sh)
+            if st:
+                raise RuntimeError(f"library error {st}")
     else:
         T, P = Skv, 1
 
@@ -314,24 +380,26 @@ def main():
                 "kernel": kernel, "algorithmic_bytes_per_launch": alg}
         value = kv / (ms_step * 1e-3) / 1e9
         unit = "GB/s"
-        unit_fn = lambda batches: kv * batches / 1e9  # noqa: E731
+        unit_fn = lambda frac: kv * frac / 1e9  # noqa: E731
     else:
-        kernel = "attn_mfma" + ("_local" if cfg.local else "")
+        kernel = "attn_mfma" + ("_local" if cfg.local else "") + (
+            ("_split_diff" if P > 1 else "_diff") if cfg.diff else "")
         src = source_hash("attn_mfma.hip", "ef_device.hpp")
-        flops = cfg.flops()
+        # The differential layer launches the attention kernel once per branch.
+        flops = cfg.flops() // (2 if cfg.diff else 1)
         achieved = flops / (prod_avg * 1e-3) / 1e12
         traffic = load_traffic(f"{kernel}_{cfg.name}", src, 1)
         roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
                 "traffic": traffic, "kernel": kernel, "algorithmic_flops_per_launch": flops}
-        value = flops / (ms_step * 1e-3) / 1e12
+        value = cfg.flops() / (ms_step * 1e-3) / 1e12
         unit = "TFLOP/s"
-        unit_fn = lambda batches: flops * batches / 1e12  # noqa: E731
+        unit_fn = lambda frac: cfg.flops() * frac / 1e12  # noqa: E731
 
     cpu = None
     if args.cpu_seconds > 0:
         print("[bench] timing the fp64 oracle on the host", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(cfg, q_cpu, k_cpu, v_cpu, args.cpu_seconds, unit_fn)
+        cpu = cpu_baseline(cfg, cpu_inputs, args.cpu_seconds, unit_fn)
         cpu["unit"] = unit
 
     out = {
@@ -348,7 +416,9 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (seeded i.i.d. N(0,1) bf16 q/k/v)",
         "config": {"workload": cfg.name, "B": B, "Hq": Hq, "Hkv": Hkv, "Sq": Sq, "Skv": Skv,
-                   "D": D, "causal": bool(cfg.causal), "window": W, "sinks": S, "partition_size": T if decode else None,
+                   "D": D, "causal": bool(cfg.causal), "window": W, "sinks": S,
+                   "differential": cfg.diff,
+                   "partition_size": T if (decode or cfg.diff) else None,
                    "partitions": P, "kv_buffer_sets": nbuf, "parallelism": "single GPU"},
         "roofline": roof,
         "cpu_baseline": cpu,

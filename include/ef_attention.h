@@ -66,7 +66,8 @@ typedef enum {
   EF_ERR_WORKSPACE_TOO_SMALL = 7,  /* workspace is NULL or smaller than required */
   EF_ERR_INVALID_SCALE = 8,        /* scale is NaN or infinite */
   EF_ERR_HIP = 9,                  /* HIP reported an error when the work was enqueued */
-  EF_ERR_INVALID_MASK = 10         /* local attention: window < 1 or sinks < 0 */
+  EF_ERR_INVALID_MASK = 10,        /* local attention: window < 1 or sinks < 0 */
+  EF_ERR_INVALID_DIFF = 11         /* differential attention: lambda_init or eps not finite, or eps < 0 */
 } ef_status;
 
 /* Version of this ABI (EF_ABI_VERSION). */
@@ -248,6 +249,50 @@ ef_status ef_attention_splitkv_tune(const void* q, const void* k, const void* v,
                                     float scale, int causal, int window, int sinks,
                                     void* workspace, size_t workspace_bytes, void* stream,
                                     int* partition_size);
+
+/*
+ * Differential attention (section 7.3, the differential attention layer of
+ * the cited differential transformer): two attention branches over one value
+ * tensor,
+ *   A1 = attention(q1, k1, v),  A2 = attention(q2, k2, v)
+ * (same scale, causal flag and grouped-query mapping as ef_attention_fwd),
+ * mixed with the learned weight
+ *   lambda = exp(<lambda_q1, lambda_k1>) - exp(<lambda_q2, lambda_k2>) + lambda_init
+ * and normalised per head and query row over the head dimension:
+ *   y = A1 - lambda * A2
+ *   o = (1 - lambda_init) * norm_weight * y / sqrt(mean(y^2) + eps),
+ * and o = 0 for a row where mean(y^2) + eps is 0 (y = 0 with eps = 0). The
+ * weight, the difference and the normalisation are applied by one kernel as
+ * the first branch's output is formed, so no A1 tensor is written.
+ *   q1, q2 : [B][Hq][Sq][D] bf16; k1, k2, v : [B][Hkv][Skv][D] bf16;
+ *   o      : [B][Hq][Sq][D] fp32, also used to hold A2 between the branches.
+ *   lambda_q1, lambda_k1, lambda_q2, lambda_k2, norm_weight : [D] fp32 device
+ *            buffers, shared by all heads; norm_weight 16-byte aligned.
+ *   lambda_init, eps : finite, eps >= 0 (else EF_ERR_INVALID_DIFF).
+ *   partition_size : 0 (model choice, as for ef_attention_splitkv) or a
+ *            positive multiple of 64. When the resolved partition covers every
+ *            key each branch is one single-pass launch and the workspace is not
+ *            used (it may be NULL); otherwise each branch runs the split-KV
+ *            producer into `workspace` (ef_diff_attention_workspace_size bytes,
+ *            16-byte aligned, reused by both branches) and its combine.
+ * Other errors as for ef_attention_splitkv; all buffers are caller-owned and
+ * the call is asynchronous on `stream`.
+ */
+ef_status ef_diff_attention(const void* q1, const void* q2, const void* k1, const void* k2,
+                            const void* v, float* o, const float* lambda_q1,
+                            const float* lambda_k1, const float* lambda_q2,
+                            const float* lambda_k2, const float* norm_weight, float lambda_init,
+                            float eps, int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                            float scale, int causal, int partition_size, void* workspace,
+                            size_t workspace_bytes, void* stream);
+
+/*
+ * Workspace bytes ef_diff_attention needs for this shape and partition_size:
+ * 0 when the resolved partition covers every key (single pass), else the
+ * split-KV workspace of one branch. Returns 0 for invalid arguments too.
+ */
+size_t ef_diff_attention_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                        int partition_size);
 
 #ifdef __cplusplus
 }

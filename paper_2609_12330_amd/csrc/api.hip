@@ -178,7 +178,8 @@ ef_status from_hip(hipError_t e) { return e == hipSuccess ? EF_OK : EF_ERR_HIP; 
 
 ef_status launch_mfma(const Shape& s, const void* q, const void* k, const void* v, float* o,
                       float* ws_m, float* ws_l, float* ws_acc, int T, int P, float scale,
-                      int causal, const ef::KeyRuns& runs, hipStream_t stream) {
+                      int causal, const ef::KeyRuns& runs, hipStream_t stream,
+                      const ef::DiffParams* diff = nullptr) {
   ef::MfmaParams a{};
   a.q = static_cast<const uint16_t*>(q);
   a.k = static_cast<const uint16_t*>(k);
@@ -197,6 +198,7 @@ ef_status launch_mfma(const Shape& s, const void* q, const void* k, const void* 
   a.c_abs = std::fabs(scale) * ef::kLog2e;
   a.causal = causal ? 1 : 0;
   a.runs = runs;
+  if (diff != nullptr) a.diff = *diff;
   return from_hip(ef::launch_mfma_attention(a, scale < 0.f, stream));
 }
 
@@ -219,6 +221,7 @@ const char* ef_status_string(int status) {
     case EF_ERR_INVALID_SCALE: return "scale is not finite";
     case EF_ERR_HIP: return "HIP error while enqueueing work";
     case EF_ERR_INVALID_MASK: return "window must be >= 1 and sinks >= 0";
+    case EF_ERR_INVALID_DIFF: return "lambda_init and eps must be finite and eps >= 0";
     default: return "unknown status";
   }
 }
@@ -539,6 +542,104 @@ ef_status ef_attention_splitkv_tune(const void* q, const void* k, const void* v,
   (void)hipEventDestroy(e1);
   if (st == EF_OK) *partition_size = cands.front();
   return st;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Number of partitions ef_diff_attention uses (1 = single pass), or 0 for an
+// invalid shape or partition size.
+long long diff_partitions(const Shape& s, int partition_size, int* T_out) {
+  if (check_shape(s) != EF_OK) return 0;
+  if (partition_size < 0 || partition_size % kTileKeys != 0) return 0;
+  if (s.rows() == 0 || s.Skv == 0) return 1;
+  const int T = resolve_partition(s, s.Skv, partition_size);
+  *T_out = T;
+  return (s.Skv + (long long)T - 1) / T;
+}
+
+// One branch through the split-KV producer and the combine; with `diff` the
+// combine applies the differential epilogue against the A2 already in o.
+ef_status diff_branch_split(const Shape& s, const void* q, const void* k, const void* v, float* o,
+                            float scale, int causal, const ef::KeyRuns& runs, int T, int P,
+                            const WsLayout& w, char* ws, const ef::DiffParams* diff,
+                            hipStream_t hs) {
+  float* ws_m = reinterpret_cast<float*>(ws + w.m_off);
+  float* ws_l = reinterpret_cast<float*>(ws + w.l_off);
+  float* ws_acc = reinterpret_cast<float*>(ws + w.acc_off);
+  ef_status st = split_produce(s, q, k, v, scale, causal, runs, T, P, ws_m, ws_l, ws_acc, nullptr,
+                               nullptr, hs);
+  if (st != EF_OK) return st;
+  ef::CombineParams c{};
+  c.m = ws_m;
+  c.l = ws_l;
+  c.acc = ws_acc;
+  c.o = o;
+  c.rows = (int)s.rows();
+  c.P = P;
+  c.D = s.D;
+  if (diff != nullptr) c.diff = *diff;
+  return from_hip(ef::launch_combine(c, hs));
+}
+
+}  // namespace
+
+extern "C" {
+
+ef_status ef_diff_attention(const void* q1, const void* q2, const void* k1, const void* k2,
+                            const void* v, float* o, const float* lambda_q1,
+                            const float* lambda_k1, const float* lambda_q2,
+                            const float* lambda_k2, const float* norm_weight, float lambda_init,
+                            float eps, int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                            float scale, int causal, int partition_size, void* workspace,
+                            size_t workspace_bytes, void* stream) {
+  const Shape s{B, Hq, Hkv, Sq, Skv, D};
+  ef_status st = check_shape(s);
+  if (st != EF_OK) return st;
+  if (partition_size < 0 || partition_size % kTileKeys != 0) return EF_ERR_INVALID_PARTITION;
+  st = check_io(s, q1, k1, v, o, scale);
+  if (st != EF_OK) return st;
+  st = check_io(s, q2, k2, v, o, scale);
+  if (st != EF_OK) return st;
+  if (!std::isfinite(lambda_init) || !std::isfinite(eps) || eps < 0.f) return EF_ERR_INVALID_DIFF;
+  if (s.rows() == 0) return EF_OK;
+  if (lambda_q1 == nullptr || lambda_k1 == nullptr || lambda_q2 == nullptr ||
+      lambda_k2 == nullptr || norm_weight == nullptr)
+    return EF_ERR_NULL_POINTER;
+  if (misaligned(norm_weight)) return EF_ERR_MISALIGNED;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  // No keys: A1 = A2 = 0, so y = 0 and every output row is 0.
+  if (s.Skv == 0) return from_hip(ef::launch_zero_fill(o, (size_t)s.rows() * s.D, hs));
+  int T = 0;
+  const long long P = diff_partitions(s, partition_size, &T);
+  if (P > kMaxGridYZ) return EF_ERR_INVALID_PARTITION;
+  const ef::DiffParams diff{lambda_q1, lambda_k1, lambda_q2, lambda_k2, norm_weight, lambda_init,
+                            eps};
+  const ef::KeyRuns runs = key_runs(Sq, Skv, 0, 0);
+  if (P == 1) {
+    st = launch_mfma(s, q2, k2, v, o, nullptr, nullptr, nullptr, runs.lv, 1, scale, causal, runs,
+                     hs);
+    if (st != EF_OK) return st;
+    return launch_mfma(s, q1, k1, v, o, nullptr, nullptr, nullptr, runs.lv, 1, scale, causal,
+                       runs, hs, &diff);
+  }
+  const WsLayout w = ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv);
+  if (workspace == nullptr || workspace_bytes < w.bytes) return EF_ERR_WORKSPACE_TOO_SMALL;
+  if (misaligned(workspace)) return EF_ERR_MISALIGNED;
+  char* ws = static_cast<char*>(workspace);
+  st = diff_branch_split(s, q2, k2, v, o, scale, causal, runs, T, (int)P, w, ws, nullptr, hs);
+  if (st != EF_OK) return st;
+  return diff_branch_split(s, q1, k1, v, o, scale, causal, runs, T, (int)P, w, ws, &diff, hs);
+}
+
+size_t ef_diff_attention_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                        int partition_size) {
+  const Shape s{B, Hq, Hkv, Sq, Skv, D};
+  int T = 0;
+  const long long P = diff_partitions(s, partition_size, &T);
+  if (P <= 1) return 0;
+  return ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv).bytes;
 }
 
 }  // extern "C"

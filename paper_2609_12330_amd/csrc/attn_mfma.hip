@@ -44,6 +44,13 @@
 // [0, S) and those from the window start of the workgroup's first row to its
 // causal end. Both runs feed the same rolling reducer, so the sink and window
 // keys share one softmax normalisation; the keys in between are never read.
+//
+// Differential attention (section 7.3), single pass: the launch for the first
+// branch finds the second branch's output in o, and its epilogue forms
+// y = A1 - lambda * A2 from the carried value, mixes in lambda from the four
+// learned vectors, RMS-normalises the row over D (the two lanes of a query
+// hold its two halves) and writes the result, so A1 never reaches HBM.
+#include "diff_norm.hpp"
 #include "ef_device.hpp"
 #include "ef_kernels.hpp"
 
@@ -305,7 +312,7 @@ __device__ __forceinline__ void pipelined_step(
   __syncthreads();
 }
 
-template <int D, int NW, bool NEG>
+template <int D, int NW, bool NEG, bool DIFF = false>
 __global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(kWavesPerEu<NW>)))
 void attn_mfma_kernel(MfmaParams a) {
   using Geo = TileGeom<D>;
@@ -444,6 +451,44 @@ void attn_mfma_kernel(MfmaParams a) {
 
   // Row sum over both lane halves.
   const float ltot = lsum + __shfl_xor(lsum, 32, 64);
+  if constexpr (DIFF) {
+    // Differential attention, first branch (section 7.3): mix with the second
+    // branch's output already in o and normalise the row. Lanes l and l ^ 32
+    // hold the two halves of a row.
+    const float lam = diff_lambda(a.diff, lane, D);
+    const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
+    const float* prev = a.o + orow * D;
+    float ss = 0.f;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int d = dt * 32 + 8 * q4 + 4 * h;
+        const float4 a2 = rvalid ? *reinterpret_cast<const float4*>(prev + d)
+                                 : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float a2v[4] = {a2.x, a2.y, a2.z, a2.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float y = fmaf(-lam, a2v[e], oacc[dt][4 * q4 + e] * inv);
+          oacc[dt][4 * q4 + e] = y;
+          ss = fmaf(y, y, ss);
+        }
+      }
+    const float rn = diff_row_factor(a.diff, ss + __shfl_xor(ss, 32, 64), D);
+    if (!rvalid) return;
+    float* orp = a.o + orow * D;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+      for (int q4 = 0; q4 < 4; ++q4) {
+        const int d = dt * 32 + 8 * q4 + 4 * h;
+        const float4 gw = *reinterpret_cast<const float4*>(a.diff.gamma + d);
+        *reinterpret_cast<float4*>(orp + d) =
+            make_float4(rn * gw.x * oacc[dt][4 * q4], rn * gw.y * oacc[dt][4 * q4 + 1],
+                        rn * gw.z * oacc[dt][4 * q4 + 2], rn * gw.w * oacc[dt][4 * q4 + 3]);
+      }
+    return;
+  }
   if (!rvalid) return;
   if (a.ws_m == nullptr) {
     const float inv = ltot > 0.f ? 1.f / ltot : 0.f;
@@ -477,10 +522,10 @@ void attn_mfma_kernel(MfmaParams a) {
   }
 }
 
-template <int D, int NW, bool NEG>
+template <int D, int NW, bool NEG, bool DIFF>
 hipError_t launch_one(const MfmaParams& a, hipStream_t stream) {
   const size_t lds = TileGeom<D>::LDS_BYTES;
-  auto kern = attn_mfma_kernel<D, NW, NEG>;
+  auto kern = attn_mfma_kernel<D, NW, NEG, DIFF>;
   // More than 64 KiB of LDS per workgroup needs the attribute; set once per kernel.
   static const hipError_t attr = hipFuncSetAttribute(
       reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -492,7 +537,9 @@ hipError_t launch_one(const MfmaParams& a, hipStream_t stream) {
 
 template <int D, int NW>
 hipError_t launch_nw(const MfmaParams& a, bool neg, hipStream_t stream) {
-  return neg ? launch_one<D, NW, true>(a, stream) : launch_one<D, NW, false>(a, stream);
+  if (a.diff.gamma != nullptr)
+    return neg ? launch_one<D, NW, true, true>(a, stream) : launch_one<D, NW, false, true>(a, stream);
+  return neg ? launch_one<D, NW, true, false>(a, stream) : launch_one<D, NW, false, false>(a, stream);
 }
 
 }  // namespace

@@ -12,6 +12,7 @@
 // side is rescaled by exp of the difference; the identity state (-inf, 0, 0)
 // contributes nothing), then the 32 partition lanes of each half merge
 // pairwise in a fixed butterfly order, so the result is deterministic.
+#include "diff_norm.hpp"
 #include "ef_device.hpp"
 #include "ef_kernels.hpp"
 
@@ -82,8 +83,11 @@ __global__ __launch_bounds__(64) void combine_sliced_kernel(CombineParams a) {
 }
 
 // Few partitions: one wave per row, each lane owning D/64 adjacent elements and
-// folding the row's partitions in order.
-template <int D>
+// folding the row's partitions in order. With DIFF the states are the first
+// branch of a differential attention layer: the wave also forms
+// y = A1 - lambda * A2 against the second branch's output already in o and
+// writes the RMS-normalised row (section 7.3).
+template <int D, bool DIFF>
 __global__ __launch_bounds__(256) void combine_rows_kernel(CombineParams a) {
   constexpr int EPL = D / 64;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
@@ -113,19 +117,34 @@ __global__ __launch_bounds__(256) void combine_rows_kernel(CombineParams a) {
     M = mn;
   }
   const float inv = (M == kNegInf || L == 0.f) ? 0.f : 1.f / L;
+  float* orow = a.o + (size_t)row * D + lane * EPL;
+  if constexpr (DIFF) {
+    const float lam = diff_lambda(a.diff, lane, D);
+    float ss = 0.f;
 #pragma unroll
-  for (int e = 0; e < EPL; ++e) a.o[(size_t)row * D + lane * EPL + e] = A[e] * inv;
+    for (int e = 0; e < EPL; ++e) {
+      A[e] = fmaf(-lam, orow[e], A[e] * inv);
+      ss = fmaf(A[e], A[e], ss);
+    }
+    const float rn = diff_row_factor(a.diff, wave_sum(ss), D);
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) orow[e] = rn * a.diff.gamma[lane * EPL + e] * A[e];
+  } else {
+#pragma unroll
+    for (int e = 0; e < EPL; ++e) orow[e] = A[e] * inv;
+  }
 }
 
 hipError_t launch_combine(const CombineParams& a, hipStream_t stream) {
   if (a.rows == 0) return hipSuccess;
-  if (a.P <= kRowsKernelMaxP) {
+  const bool diff = a.diff.gamma != nullptr;
+  if (a.P <= kRowsKernelMaxP || diff) {
+    // The differential epilogue normalises whole rows, so it always takes the
+    // one-wave-per-row layout.
     const unsigned blocks = (unsigned)((a.rows + 3) / 4);
-    if (a.D == 128) {
-      hipLaunchKernelGGL(combine_rows_kernel<128>, dim3(blocks), dim3(256), 0, stream, a);
-    } else {
-      hipLaunchKernelGGL(combine_rows_kernel<64>, dim3(blocks), dim3(256), 0, stream, a);
-    }
+    auto kern = a.D == 128 ? (diff ? combine_rows_kernel<128, true> : combine_rows_kernel<128, false>)
+                           : (diff ? combine_rows_kernel<64, true> : combine_rows_kernel<64, false>);
+    hipLaunchKernelGGL(kern, dim3(blocks), dim3(256), 0, stream, a);
   } else {
     const size_t waves = (size_t)a.rows * (a.D / kSlice);
     hipLaunchKernelGGL(combine_sliced_kernel, dim3((unsigned)waves), dim3(64), 0, stream, a);

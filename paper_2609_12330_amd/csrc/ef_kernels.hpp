@@ -16,6 +16,19 @@ struct KeyRuns {
   int window, sinks;  // window > 0: key j visible to row i iff j > n_i - window or j < sinks
 };
 
+// Differential attention epilogue (section 7.3): the output row is
+// (1 - lambda_init) * gamma * y / sqrt(mean(y^2) + eps) with y = A1 - lambda * A2
+// and lambda = exp(<lq1, lk1>) - exp(<lq2, lk2>) + lambda_init. Unused while
+// gamma is null.
+struct DiffParams {
+  const float* lq1;
+  const float* lk1;
+  const float* lq2;
+  const float* lk2;
+  const float* gamma;  // [D] fp32 each
+  float lambda_init, eps;
+};
+
 // Split-KV decode producer (VALU path, G*Sq <= 8 query rows per kv head).
 struct DecodeParams {
   const uint16_t* q;  // [B][Hq][Sq][D] bf16
@@ -61,6 +74,9 @@ struct MfmaParams {
   float c_abs;   // |scale| * log2(e)
   int causal;
   KeyRuns runs;  // split mode: partitions cover the virtual key axis
+  // Differential attention, single pass only: with diff.gamma set this launch
+  // is the first branch and o already holds the second branch's output.
+  DiffParams diff;
 };
 
 // Combine of stored partial states.
@@ -70,6 +86,9 @@ struct CombineParams {
   const float* acc;
   float* o;  // [rows][D]
   int rows, P, D;
+  // Differential attention: with diff.gamma set the states are the first
+  // branch's and o already holds the second branch's output.
+  DiffParams diff;
 };
 
 // Fill of an fp32 buffer with zeros (output rows that see no key).

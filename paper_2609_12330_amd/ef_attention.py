@@ -30,6 +30,7 @@ STATUS_NAMES = {
     8: "EF_ERR_INVALID_SCALE",
     9: "EF_ERR_HIP",
     10: "EF_ERR_INVALID_MASK",
+    11: "EF_ERR_INVALID_DIFF",
 }
 
 # Exported symbols and their C signatures (restype, argtypes).
@@ -53,6 +54,9 @@ SIGNATURES = {
     "ef_attention_splitkv_modeled_us": (ctypes.c_double, [_i, _i, _i, _i, _i, _i, _i, _i, _i]),
     "ef_attention_splitkv_tune": (_i, [_vp, _vp, _vp, _fp, _i, _i, _i, _i, _i, _i, _f, _i, _i, _i,
                                        _vp, _sz, _vp, ctypes.POINTER(ctypes.c_int)]),
+    "ef_diff_attention": (_i, [_vp, _vp, _vp, _vp, _vp, _fp, _fp, _fp, _fp, _fp, _fp, _f, _f, _i,
+                               _i, _i, _i, _i, _i, _f, _i, _i, _vp, _sz, _vp]),
+    "ef_diff_attention_workspace_size": (_sz, [_i, _i, _i, _i, _i, _i, _i]),
 }
 
 
@@ -112,6 +116,19 @@ def ef_attention_splitkv_partials(q, k, v, B, Hq, Hkv, Sq, Skv, D, scale, causal
     return _lib().ef_attention_splitkv_partials(q, k, v, B, Hq, Hkv, Sq, Skv, D, scale,
                                                 int(causal), partition_size, workspace,
                                                 workspace_bytes, stream)
+
+
+def ef_diff_attention(q1, q2, k1, k2, v, o, lambda_q1, lambda_k1, lambda_q2, lambda_k2,
+                      norm_weight, lambda_init, eps, B, Hq, Hkv, Sq, Skv, D, scale, causal,
+                      partition_size, workspace, workspace_bytes, stream) -> int:
+    return _lib().ef_diff_attention(q1, q2, k1, k2, v, o, lambda_q1, lambda_k1, lambda_q2,
+                                    lambda_k2, norm_weight, lambda_init, eps, B, Hq, Hkv, Sq, Skv,
+                                    D, scale, int(causal), partition_size, workspace,
+                                    workspace_bytes, stream)
+
+
+def ef_diff_attention_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size) -> int:
+    return _lib().ef_diff_attention_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size)
 
 
 def ef_attention_combine(m, l, acc, o, rows, num_partitions, D, stream) -> int:
@@ -406,3 +423,40 @@ def tune_partition_size(q, k, v, scale: Optional[float] = None, causal: bool = F
                                    _stream_handle(stream), t)
     _check(st, "ef_attention_splitkv_tune")
     return int(t.value)
+
+
+def diff_attention(q1, q2, k1, k2, v, lambda_q1, lambda_k1, lambda_q2, lambda_k2, norm_weight,
+                   lambda_init: float, eps: float = 1e-5, scale: Optional[float] = None,
+                   causal: bool = False, partition_size: int = 0, workspace=None, out=None,
+                   stream=None):
+    """Differential attention through ef_diff_attention: (1 - lambda_init) * RMSNorm(A1 - lambda
+    A2) with A1 = attention(q1, k1, v), A2 = attention(q2, k2, v) and lambda = exp(<lq1, lk1>) -
+    exp(<lq2, lk2>) + lambda_init; the four lambda vectors and norm_weight are fp32 [D]."""
+    torch = _torch()
+    B, Hq, Hkv, Sq, Skv, D = _check_qkv(q1, k1, v)
+    if _check_qkv(q2, k2, v) != (B, Hq, Hkv, Sq, Skv, D):
+        raise ValueError("q2 and k2 must be shaped like q1 and k1")
+    for name, t in (("q2", q2), ("k1", k1), ("k2", k2), ("v", v)):
+        _same_device(t, q1, name)
+    vecs = (lambda_q1, lambda_k1, lambda_q2, lambda_k2, norm_weight)
+    for name, t in zip(("lambda_q1", "lambda_k1", "lambda_q2", "lambda_k2", "norm_weight"), vecs):
+        if t.dtype != torch.float32 or t.shape != (D,) or not t.is_contiguous():
+            raise ValueError(f"{name} must be a contiguous fp32 [D] tensor")
+        _same_device(t, q1, name)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    o = _out(q1, out)
+    need = int(ef_diff_attention_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size))
+    if workspace is None and need > 0:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q1.device)
+    if workspace is not None:
+        _check_workspace(workspace, q1)
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    else:
+        ws_ptr, ws_bytes = None, 0
+    st = ef_diff_attention(q1.data_ptr(), q2.data_ptr(), k1.data_ptr(), k2.data_ptr(),
+                           v.data_ptr(), o.data_ptr(), *(t.data_ptr() for t in vecs),
+                           float(lambda_init), float(eps), B, Hq, Hkv, Sq, Skv, D, float(scale),
+                           causal, partition_size, ws_ptr, ws_bytes, _stream_handle(stream))
+    _check(st, "ef_diff_attention")
+    return o

@@ -13,6 +13,8 @@ suites are not available, so these i.i.d. N(0, 1) tensors of the same layout
 stand in for them. The local-attention workloads follow the sliding-window GQA
 (1, 4096, 16K) and attention-sink (1, 1024, 32K) layers of section 7.3, read
 as (batch, query tokens, key tokens) with a 4096-key window and 4 sink keys.
+The differential-attention workload is that section's (1, 1024, 32K) layer
+with 32 heads of 128; its inputs are drawn by :func:`make_diff_inputs`.
 """
 
 from __future__ import annotations
@@ -41,6 +43,7 @@ class AttentionConfig:
     scale: float = dataclasses.field(default=float("nan"))
     window: int = 0  # local attention: keys j > n_i - window are visible (causal only)
     sinks: int = 0   # ... and keys j < sinks
+    diff: bool = False  # differential attention: two q/k branches over one v
 
     @property
     def local(self) -> bool:
@@ -86,17 +89,21 @@ class AttentionConfig:
         return (n_hi + 1 - lo) + min(self.sinks, lo)
 
     def flops(self) -> int:
-        """Algorithmic flops: 2*D for q.k plus 2*D for p*v per visible pair."""
-        return 4 * self.D * self.visible_pairs()
+        """Algorithmic flops: 2*D for q.k plus 2*D for p*v per visible pair (per branch of a
+        differential layer)."""
+        return (8 if self.diff else 4) * self.D * self.visible_pairs()
 
     def kv_bytes(self) -> int:
         """K and V bytes of every key some query row can see, read once."""
         return 2 * self.B * self.Hkv * self.visible_keys() * self.D * 2
 
     def algorithmic_bytes(self) -> int:
-        """bf16 q, k, v read once plus the fp32 output written once."""
+        """bf16 q, k, v read once plus the fp32 output written once (differential: both
+        branches' q and k, the shared v)."""
         q = self.B * self.Hq * self.Sq * self.D * 2
         o = self.B * self.Hq * self.Sq * self.D * 4
+        if self.diff:
+            return 2 * q + 3 * self.kv_bytes() // 2 + o
         return q + self.kv_bytes() + o
 
 
@@ -131,7 +138,14 @@ LOCAL_CONFIGS: Tuple[AttentionConfig, ...] = (
                     causal=True, window=4096, sinks=4),
 )
 
-ALL_CONFIGS: Tuple[AttentionConfig, ...] = CONFIGS + LOCAL_CONFIGS
+# Differential attention (section 7.3): the (1, 1024, 32K) layer as 32 heads of
+# 128 over 1024 new tokens of a 32K context (bottom-right causal mask).
+DIFF_CONFIGS: Tuple[AttentionConfig, ...] = (
+    AttentionConfig("diff_attn_b1_h32_q1024_kv32768_d128", 1, 32, 32, 1024, 32768, 128,
+                    causal=True, diff=True),
+)
+
+ALL_CONFIGS: Tuple[AttentionConfig, ...] = CONFIGS + LOCAL_CONFIGS + DIFF_CONFIGS
 
 CONFIG_BY_NAME: Dict[str, AttentionConfig] = {c.name: c for c in ALL_CONFIGS}
 
@@ -155,6 +169,26 @@ def make_shape_inputs(B, Hq, Hkv, Sq, Skv, D, seed, q_mult=1.0):
     """Same recipe as :func:`make_inputs` for an arbitrary shape."""
     cfg = AttentionConfig("adhoc", B, Hq, Hkv, Sq, Skv, D, causal=False, q_mult=q_mult)
     return make_inputs(cfg, seed)
+
+
+# Differential attention constants of the synthetic layer: the mixing weight's
+# initial value and the RMS norm epsilon.
+DIFF_LAMBDA_INIT = 0.8
+DIFF_EPS = 1e-5
+
+
+def make_diff_inputs(B, Hq, Hkv, Sq, Skv, D, seed):
+    """Differential attention inputs on the CPU, in this order from one generator:
+    q1, q2 [B,Hq,Sq,D] and k1, k2, v [B,Hkv,Skv,D] as bf16(N(0,1)); then the four fp32 [D]
+    mixing vectors lambda_q1, lambda_k1, lambda_q2, lambda_k2 ~ N(0, 0.1^2) and the fp32 [D]
+    norm weight 1 + 0.1 N(0,1). Returns (q1, q2, k1, k2, v, (lq1, lk1, lq2, lk2), gamma)."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(int(seed))
+    q1, q2 = (torch.randn(B, Hq, Sq, D, generator=g).to(torch.bfloat16) for _ in range(2))
+    k1, k2, v = (torch.randn(B, Hkv, Skv, D, generator=g).to(torch.bfloat16) for _ in range(3))
+    lam = tuple(0.1 * torch.randn(D, generator=g) for _ in range(4))
+    gamma = 1.0 + 0.1 * torch.randn(D, generator=g)
+    return q1, q2, k1, k2, v, lam, gamma
 
 
 def to_f64(t: torch.Tensor):

@@ -54,7 +54,7 @@ def test_library_exports_every_header_symbol():
 @needs_lib
 def test_status_strings():
     lib = ef.library()
-    for s in range(0, 11):
+    for s in range(0, 12):
         assert lib.ef_status_string(s)
         assert lib.ef_status_string(s) != b"unknown status"
     assert lib.ef_status_string(0) == b"ok"
@@ -96,9 +96,20 @@ def split_local(window=64, sinks=4, **kw):
                                          sinks, a["T"], a["ws"], a["wsb"], a["stream"])
 
 
+def diff(**kw):
+    a = dict(q=A, q2=A, k=A, k2=A, v=A, o=A, lq1=A, lk1=A, lq2=A, lk2=A, gamma=A, li=0.2,
+             eps=1e-5, B=1, Hq=4, Hkv=2, Sq=8, Skv=16, D=128, scale=0.1, causal=0, T=0, ws=None,
+             wsb=0, stream=None)
+    a.update(kw)
+    return ef.ef_diff_attention(a["q"], a["q2"], a["k"], a["k2"], a["v"], a["o"], a["lq1"],
+                                a["lk1"], a["lq2"], a["lk2"], a["gamma"], a["li"], a["eps"],
+                                a["B"], a["Hq"], a["Hkv"], a["Sq"], a["Skv"], a["D"], a["scale"],
+                                a["causal"], a["T"], a["ws"], a["wsb"], a["stream"])
+
+
 @needs_lib
-@pytest.mark.parametrize("call", [fwd, split, fwd_local, split_local],
-                         ids=["fwd", "splitkv", "fwd_local", "splitkv_local"])
+@pytest.mark.parametrize("call", [fwd, split, fwd_local, split_local, diff],
+                         ids=["fwd", "splitkv", "fwd_local", "splitkv_local", "diff"])
 def test_validation_errors(call):
     assert call(D=96) == 4
     assert call(D=0) == 4
@@ -154,6 +165,35 @@ def test_splitkv_specific_validation():
     need = ef.ef_attention_splitkv_workspace_size(1, 4, 2, 1, 1000, 128, 256)
     assert split(wsb=need - 1) == 7
     assert split(ws=MIS, wsb=need) == 5
+
+
+@needs_lib
+def test_diff_specific_validation():
+    assert diff(li=math.nan) == 11
+    assert diff(li=math.inf) == 11
+    assert diff(eps=-1e-6) == 11
+    assert diff(eps=math.inf) == 11
+    assert diff(eps=math.nan) == 11
+    for name in ("q2", "k2", "lq1", "lk1", "lq2", "lk2", "gamma"):
+        assert diff(**{name: None}) == 1, name
+    assert diff(q2=MIS) == 5
+    assert diff(k2=MIS) == 5
+    assert diff(gamma=MIS) == 5
+    assert diff(T=100) == 6
+    assert diff(T=-64) == 6
+    # Skv = 1000 in 256-key partitions: split, so the workspace is required.
+    need = ef.ef_diff_attention_workspace_size(1, 4, 2, 8, 1000, 128, 256)
+    assert need == ef.ef_attention_splitkv_workspace_size(1, 4, 2, 8, 1000, 128, 256) > 0
+    assert diff(Skv=1000, T=256) == 7
+    assert diff(Skv=1000, T=256, ws=A, wsb=need - 1) == 7
+    assert diff(Skv=1000, T=256, ws=MIS, wsb=need) == 5
+    # One partition covering every key: single pass, no workspace.
+    assert ef.ef_diff_attention_workspace_size(1, 4, 2, 8, 1000, 128, 1024) == 0
+    assert ef.ef_diff_attention_workspace_size(1, 4, 2, 8, 0, 128, 256) == 0
+    assert ef.ef_diff_attention_workspace_size(1, 4, 2, 8, 1000, 96, 256) == 0
+    assert ef.ef_diff_attention_workspace_size(1, 4, 2, 8, 1000, 128, 100) == 0
+    # Nothing to compute: accepted, the lambda vectors are not needed.
+    assert diff(B=0, lq1=None, gamma=None) == 0
 
 
 @needs_lib

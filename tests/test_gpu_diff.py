@@ -1,0 +1,173 @@
+"""GPU parity of differential attention (section 7.3: two attention branches
+sharing v, their learned weighted difference RMS-normalised per head) through
+the C ABI against the fp64 oracle, with the bar of the other parity tests:
+max |o - ref| <= 1e-2 and mean |o - ref| <= 1e-3 over every compared output.
+The single-pass path (one partition) fuses the epilogue into the first
+branch's attention kernel; the split path fuses it into the first branch's
+combine. Every case prints its name before it touches the GPU.
+"""
+
+import math
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2609_12330_amd import ef_attention as ef
+from paper_2609_12330_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS = 1e-2
+MEAN_ABS = 1e-3
+
+
+def announce(msg):
+    print(f"[gpu case] {msg}", file=sys.stderr, flush=True)
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    if not os.path.exists(ef.LIB_PATH):
+        raise RuntimeError("libef_attention.so is not built; the HIP path must be present")
+    ef.library()
+    yield
+
+
+def f64(t):
+    return t.detach().cpu().double().numpy()
+
+
+def assert_close(o, ref, what):
+    o = o.detach().cpu().double().numpy() if isinstance(o, torch.Tensor) else o
+    assert np.isfinite(o).all(), f"{what}: non-finite output"
+    d = np.abs(o - ref)
+    mx, mean = float(d.max()) if d.size else 0.0, float(d.mean()) if d.size else 0.0
+    assert mx <= MAX_ABS and mean <= MEAN_ABS, f"{what}: max {mx:.3e} mean {mean:.3e}"
+
+
+def run_gpu(inp, lambda_init, eps, scale, causal, partition_size=0, workspace=None, out=None):
+    q1, q2, k1, k2, v, lam, gamma = inp
+    dev = [t.cuda() for t in (q1, q2, k1, k2, v)] + [t.cuda() for t in lam] + [gamma.cuda()]
+    return ef.diff_attention(*dev, lambda_init=lambda_init, eps=eps, scale=scale, causal=causal,
+                             partition_size=partition_size, workspace=workspace, out=out)
+
+
+def run_oracle(inp, lambda_init, eps, scale, causal):
+    q1, q2, k1, k2, v, lam, gamma = inp
+    return oracle.diff_attention_ref(f64(q1), f64(q2), f64(k1), f64(k2), f64(v), *map(f64, lam),
+                                     f64(gamma), lambda_init, eps, scale, causal)
+
+
+# B, Hq, Hkv, Sq, Skv, D, causal, partition_size (0: model choice; >= Skv: single pass)
+SMALL = [
+    (1, 4, 4, 64, 64, 64, False, 0),
+    (1, 4, 2, 100, 100, 128, True, 1024),     # single pass, ragged rows and keys
+    (2, 8, 2, 70, 333, 128, True, 64),        # split, 6 partitions
+    (1, 2, 2, 129, 65, 64, True, 1024),       # Sq > Skv: rows that see no key
+    (1, 2, 2, 129, 65, 64, True, 64),
+    (2, 8, 8, 1, 1000, 128, False, 128),      # decode rows through the split producer
+    (1, 32, 8, 1, 3000, 128, False, 64),      # 47 partitions: P > 32
+    (1, 8, 1, 5, 300, 128, True, 0),          # G = 8, few rows
+    (1, 4, 4, 300, 1000, 64, True, 256),
+    (1, 16, 2, 40, 130, 128, False, 4096),
+]
+
+
+@pytest.mark.parametrize("shape", SMALL, ids=lambda s: "x".join(map(str, s)))
+def test_diff_small(shape):
+    B, Hq, Hkv, Sq, Skv, D, causal, T = shape
+    announce(f"diff {shape}")
+    inp = wl.make_diff_inputs(B, Hq, Hkv, Sq, Skv, D, seed=700 + sum(shape))
+    scale = 1.0 / math.sqrt(D)
+    o = run_gpu(inp, 0.8, 1e-5, scale, causal, T)
+    torch.cuda.synchronize()
+    assert_close(o, run_oracle(inp, 0.8, 1e-5, scale, causal), f"diff {shape}")
+
+
+def test_diff_negative_scale_and_other_lambda():
+    announce("diff negative scale")
+    inp = wl.make_diff_inputs(1, 4, 2, 90, 200, 128, seed=711)
+    for T in (1024, 64):
+        o = run_gpu(inp, 0.3, 1e-6, -0.09, True, T)
+        torch.cuda.synchronize()
+        assert_close(o, run_oracle(inp, 0.3, 1e-6, -0.09, True), f"negative scale T={T}")
+
+
+def test_diff_zero_rows_with_zero_eps():
+    """eps = 0: equal branches with lambda = 1 give y = 0 and rows that see no key give
+    y = 0; both are zero rows, never NaN."""
+    announce("diff zero rows")
+    q1, q2, k1, k2, v, lam, gamma = wl.make_diff_inputs(1, 2, 2, 129, 65, 64, seed=712)
+    z = torch.zeros(64)
+    same = (q1, q1, k1, k1, v, (z, z, z, z), gamma)
+    for T in (1024, 64):
+        o = run_gpu(same, 1.0, 0.0, 0.125, False, T)
+        torch.cuda.synchronize()
+        assert torch.equal(o.cpu(), torch.zeros_like(o.cpu())), f"equal branches T={T}"
+        inp = (q1, q2, k1, k2, v, lam, gamma)
+        o = run_gpu(inp, 0.8, 0.0, 0.125, True, T)
+        torch.cuda.synchronize()
+        assert torch.equal(o[:, :, :64].cpu(), torch.zeros(1, 2, 64, 64)), f"masked rows T={T}"
+        assert_close(o, run_oracle(inp, 0.8, 0.0, 0.125, True), f"eps 0 T={T}")
+
+
+def test_diff_no_keys_writes_zeros():
+    announce("diff Skv = 0")
+    inp = wl.make_diff_inputs(1, 4, 2, 3, 0, 128, seed=713)
+    o = run_gpu(inp, 0.8, 1e-5, 0.1, False, 0, out=torch.full((1, 4, 3, 128), 7.0,
+                                                               device="cuda"))
+    torch.cuda.synchronize()
+    assert torch.equal(o.cpu(), torch.zeros(1, 4, 3, 128))
+
+
+def test_diff_single_pass_and_split_agree_and_repeat():
+    """Both paths against each other, and each bit-for-bit deterministic across calls."""
+    announce("diff single pass vs split")
+    inp = wl.make_diff_inputs(1, 8, 2, 200, 900, 128, seed=714)
+    one = run_gpu(inp, 0.8, 1e-5, 0.09, True, 1024)
+    two = run_gpu(inp, 0.8, 1e-5, 0.09, True, 1024)
+    s1 = run_gpu(inp, 0.8, 1e-5, 0.09, True, 128)
+    s2 = run_gpu(inp, 0.8, 1e-5, 0.09, True, 128)
+    torch.cuda.synchronize()
+    assert torch.equal(one, two) and torch.equal(s1, s2)
+    # The two paths round P and the partial states differently; each meets the parity
+    # bar against the oracle, so they agree to the same bar.
+    assert_close(one, s1.cpu().double().numpy(), "single pass vs split")
+
+
+def test_diff_invalid_arguments_write_nothing():
+    announce("diff invalid arguments")
+    q1, q2, k1, k2, v, lam, gamma = wl.make_diff_inputs(1, 4, 2, 8, 100, 128, seed=715)
+    dev = [t.cuda() for t in (q1, q2, k1, k2, v)] + [t.cuda() for t in lam] + [gamma.cuda()]
+    out = torch.full((1, 4, 8, 128), 3.0, device="cuda")
+    with pytest.raises(ef.EfError, match="EF_ERR_INVALID_DIFF"):
+        ef.diff_attention(*dev, lambda_init=float("nan"), out=out)
+    with pytest.raises(ef.EfError, match="EF_ERR_INVALID_DIFF"):
+        ef.diff_attention(*dev, lambda_init=0.8, eps=-1.0, out=out)
+    with pytest.raises(ValueError):
+        ef.diff_attention(*dev[:5], *[t[:64] for t in dev[5:9]], dev[9], lambda_init=0.8, out=out)
+    torch.cuda.synchronize()
+    assert bool((out == 3.0).all())
+
+
+def test_diff_workload_sampled_heads():
+    """The section 7.3 differential layer (1, 1024, 32K) at full size with the default
+    partition choice, as the benchmark runs it; the oracle evaluates sampled heads whole
+    (every row, every key, both branches)."""
+    cfg = wl.CONFIG_BY_NAME["diff_attn_b1_h32_q1024_kv32768_d128"]
+    announce(cfg.name)
+    inp = wl.make_diff_inputs(cfg.B, cfg.Hq, cfg.Hkv, cfg.Sq, cfg.Skv, cfg.D,
+                              wl.DEFAULT_SEED[cfg.name])
+    o = run_gpu(inp, wl.DIFF_LAMBDA_INIT, wl.DIFF_EPS, cfg.scale, True).cpu()
+    q1, q2, k1, k2, v, lam, gamma = inp
+    for h in (0, 13, 31):
+        part = (q1[:, h:h + 1], q2[:, h:h + 1], k1[:, h:h + 1], k2[:, h:h + 1], v[:, h:h + 1],
+                lam, gamma)
+        ref = run_oracle(part, wl.DIFF_LAMBDA_INIT, wl.DIFF_EPS, cfg.scale, True)
+        assert_close(o[:, h:h + 1], ref, f"{cfg.name} head {h}")

@@ -88,3 +88,24 @@ def test_local_workloads():
     assert chunk.visible_pairs() == 32 * 1024 * (4096 + 4)
     assert chunk.visible_keys() == 4096 + 1023 + 4
     assert len(set(wl.DEFAULT_SEED.values())) == len(wl.ALL_CONFIGS)
+
+
+def test_diff_workload_and_inputs():
+    cfg = wl.CONFIG_BY_NAME["diff_attn_b1_h32_q1024_kv32768_d128"]
+    assert cfg.diff and cfg.causal and (cfg.B, cfg.Hq, cfg.Hkv, cfg.Sq, cfg.Skv, cfg.D) == (
+        1, 32, 32, 1024, 32768, 128)
+    # Row i (diagonal key 31744 + i) sees 31745 + i keys; two branches of 4*D flops each.
+    pairs = 32 * sum(31745 + i for i in range(1024))
+    assert cfg.visible_pairs() == pairs and cfg.flops() == 8 * 128 * pairs
+    kv = 32 * 32768 * 128 * 2
+    assert cfg.algorithmic_bytes() == 2 * 32 * 1024 * 128 * 2 + 3 * kv + 32 * 1024 * 128 * 4
+    a = wl.make_diff_inputs(1, 4, 2, 3, 70, 64, seed=5)
+    b = wl.make_diff_inputs(1, 4, 2, 3, 70, 64, seed=5)
+    q1, q2, k1, k2, v, lam, gamma = a
+    assert q1.shape == q2.shape == (1, 4, 3, 64) and k1.shape == k2.shape == v.shape == (
+        1, 2, 70, 64)
+    assert all(t.dtype == torch.bfloat16 for t in (q1, q2, k1, k2, v))
+    assert len(lam) == 4 and all(t.dtype == torch.float32 and t.shape == (64,) for t in lam)
+    assert gamma.dtype == torch.float32 and gamma.shape == (64,)
+    assert torch.equal(q1, b[0]) and torch.equal(v, b[4]) and torch.equal(gamma, b[6])
+    assert not torch.equal(q1, q2) and not torch.equal(k1, k2)
