@@ -48,6 +48,9 @@ def parse():
     ap.add_argument("--seed", type=int, default=None)
     ap.add_argument("--partition-size", type=int, default=None,
                     help="keys per split-KV partition (default: the workload's, else the library's)")
+    ap.add_argument("--d-splits", type=int, default=None,
+                    help="output-channel slices of the channel-split decode (default: the "
+                         "workload's; 0 runs the plain split-KV path)")
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="CPU work budget of the oracle baseline (0 disables it)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -179,19 +182,28 @@ def main():
     B, Hq, Hkv, Sq, Skv, D = cfg.B, cfg.Hq, cfg.Hkv, cfg.Sq, cfg.Skv, cfg.D
 
     W, S = cfg.window, cfg.sinks
+    DS = cfg.d_splits if args.d_splits is None else args.d_splits
     if decode:
         T_req = cfg.partition_size if args.partition_size is None else args.partition_size
         T = ef.splitkv_partition_size(B, Hq, Hkv, Sq, Skv, D, T_req, W, S)
         nbytes = ef.splitkv_workspace_size(B, Hq, Hkv, Sq, Skv, D, T, W, S)
-        ws = ef.make_workspace(sets[0][0], sets[0][1], T, W, S)
+        if DS > 0:
+            nbytes = ef.ef_attention_decode_dsplit_workspace_size(B, Hq, Hkv, Sq, Skv, D, DS, T)
+        ws = torch.zeros(max(nbytes, 256), dtype=torch.uint8, device=dev)
         P = ef.splitkv_partitions(Sq, Skv, T, W, S)
         wsb = ws.numel()
         assert wsb >= nbytes
-        m, l, acc = ef.workspace_views(ws, B, Hq, Sq, Skv, D, T, W, S)
+        if DS <= 0:  # the channel split reads no workspace through these views
+            m, l, acc = ef.workspace_views(ws, B, Hq, Sq, Skv, D, T, W, S)
         rows = B * Hq * Sq
 
         def whole(q, k, v, sh):
             """The whole split-KV attention through one library call."""
+            if DS > 0:
+                return ef.ef_attention_decode_dsplit(q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                                     o.data_ptr(), B, Hq, Hkv, Sq, Skv, D,
+                                                     cfg.scale, cfg.causal, DS, T, ws.data_ptr(),
+                                                     wsb, sh)
             if cfg.local:
                 return ef.ef_attention_splitkv_local(q.data_ptr(), k.data_ptr(), v.data_ptr(),
                                                      o.data_ptr(), B, Hq, Hkv, Sq, Skv, D,
@@ -209,12 +221,13 @@ def main():
             if st:
                 raise RuntimeError(f"library error {st}")
 
-        # The library runs the combine inside the producer when G*Sq <= 8 and P <= 64;
+        # The library runs the combine inside the producer when G*Sq <= 4 and P <= 64;
         # otherwise the producer is followed by a separate combine kernel. Local
         # workloads are timed through the whole call (there is no separate local
         # producer entry point), so their "producer" figure includes any combine.
-        fused = cfg.G * Sq <= 8 and P <= 64
-        single_call = fused or cfg.local
+        valu = cfg.G * Sq <= 4 or DS > 0  # the VALU producer (else the MFMA one)
+        fused = valu and P <= 64
+        single_call = fused or cfg.local or DS > 0
 
         def step(i, ev=None):
             q, k, v = sets[i % nbuf]
@@ -367,9 +380,10 @@ def main():
     q_bytes = B * Hq * Sq * D * 2
     if decode:
         # Producer: algorithmic bytes = bf16 q + K + V read once (512 B per key per kv head).
-        kernel = ("decode_split" if cfg.Sq * cfg.G <= 8 else "attn_mfma_split") + (
-            "_local" if cfg.local else "") + ("_fused" if fused else "")
-        src = source_hash(*(("decode_split.hip", "group_combine.hpp") if cfg.Sq * cfg.G <= 8
+        kernel = ("decode_split" if valu else "attn_mfma_split") + (
+            "_local" if cfg.local else "") + (f"_dsplit{DS}" if DS > 0 else "") + (
+            "_fused" if fused and P > 1 else "")
+        src = source_hash(*(("decode_split.hip", "group_combine.hpp") if valu
                             else ("attn_mfma.hip",)), "ef_device.hpp")
         # one call: q, K, V read and o written; else the producer reads q, K, V
         alg = cfg.algorithmic_bytes() if single_call else kv + q_bytes
@@ -417,7 +431,7 @@ def main():
         "data": "synthetic (seeded i.i.d. N(0,1) bf16 q/k/v)",
         "config": {"workload": cfg.name, "B": B, "Hq": Hq, "Hkv": Hkv, "Sq": Sq, "Skv": Skv,
                    "D": D, "causal": bool(cfg.causal), "window": W, "sinks": S,
-                   "differential": cfg.diff,
+                   "differential": cfg.diff, "d_splits": DS if decode else None,
                    "partition_size": T if (decode or cfg.diff) else None,
                    "partitions": P, "kv_buffer_sets": nbuf, "parallelism": "single GPU"},
         "roofline": roof,

@@ -67,7 +67,8 @@ typedef enum {
   EF_ERR_INVALID_SCALE = 8,        /* scale is NaN or infinite */
   EF_ERR_HIP = 9,                  /* HIP reported an error when the work was enqueued */
   EF_ERR_INVALID_MASK = 10,        /* local attention: window < 1 or sinks < 0 */
-  EF_ERR_INVALID_DIFF = 11         /* differential attention: lambda_init or eps not finite, or eps < 0 */
+  EF_ERR_INVALID_DIFF = 11,        /* differential attention: lambda_init or eps not finite, or eps < 0 */
+  EF_ERR_INVALID_SPLIT = 12        /* d_splits not 1, 2 or 4, or more than 8 query rows per kv head */
 } ef_status;
 
 /* Version of this ABI (EF_ABI_VERSION). */
@@ -152,7 +153,7 @@ size_t ef_attention_splitkv_workspace_size(int B, int Hq, int Hkv, int Sq, int S
  *                      number of calls in stream order. Calls that overlap
  *                      in time must not share a workspace.
  *   workspace_bytes  : its size in bytes.
- * When G*Sq <= 8 and P <= 64 the combine runs inside the producer: the last
+ * When G*Sq <= 4 and P <= 64 the combine runs inside the producer: the last
  * workgroup of each (batch, kv head) to store its state, found with the
  * group's arrival counter, combines that group's rows and resets the counter
  * (one kernel instead of two). Otherwise a separate combine kernel follows.
@@ -226,7 +227,8 @@ ef_status ef_attention_combine(const float* m, const float* l, const float* acc,
  * states written and read) and one workgroup's streaming time times the rounds
  * of workgroups the chip holds, plus the combine, with rates measured on
  * MI355X. With partition_size = 0 the split-KV entry points take the
- * candidate (64, 128, 192, 256, 384, ... keys) this model rates fastest.
+ * candidate (64, 128, 256, 512, ... keys, and one partition holding every
+ * key) this model rates fastest.
  * Returns a negative value for invalid arguments.
  */
 double ef_attention_splitkv_modeled_us(int B, int Hq, int Hkv, int Sq, int Skv, int D,
@@ -293,6 +295,41 @@ ef_status ef_diff_attention(const void* q1, const void* q2, const void* k1, cons
  */
 size_t ef_diff_attention_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
                                         int partition_size);
+
+/*
+ * Decode with an output-channel split (section 7.2: at batch 1 the paper's
+ * selected decode kernel gives each head two blocks that compute the same
+ * scores and softmax and write different halves of the output, with no merge
+ * kernel; the N parallel refinement of the p.V product, section 4.1 and table
+ * "rules"). Each key
+ * partition of each (batch, kv head) is evaluated by d_splits workgroups:
+ * every one reads the partition's K rows and recomputes the scores, and reads,
+ * accumulates and writes only its D/d_splits value channels. The output is
+ * ef_attention_splitkv's.
+ *   q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale, causal : as ef_attention_splitkv;
+ *            at most 8 query rows per kv head ((Hq/Hkv)*Sq <= 8), else
+ *            EF_ERR_INVALID_SPLIT.
+ *   d_splits : 1, 2 or 4 (else EF_ERR_INVALID_SPLIT).
+ *   partition_size : as ef_attention_splitkv (0 = the model's choice). When it
+ *            covers every key (one partition) each workgroup writes its
+ *            channels of o directly: no workspace (it may be NULL) and no
+ *            merge. Otherwise the workspace (ef_attention_decode_dsplit_workspace_size
+ *            bytes, 16-byte aligned, counters zero on entry and left zero, as for
+ *            ef_attention_splitkv) holds the states, which every channel slice
+ *            combines for its own channels.
+ */
+ef_status ef_attention_decode_dsplit(const void* q, const void* k, const void* v, float* o,
+                                     int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                     float scale, int causal, int d_splits, int partition_size,
+                                     void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * Workspace bytes of ef_attention_decode_dsplit: 0 with one partition, else
+ * the split-KV layout with B*Hkv*d_splits counter slots. 0 for invalid
+ * arguments too.
+ */
+size_t ef_attention_decode_dsplit_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                                 int d_splits, int partition_size);
 
 #ifdef __cplusplus
 }

@@ -13,7 +13,9 @@
 namespace {
 
 constexpr int kTileKeys = 64;        // key tile of the kernels; partitions are multiples of it
-constexpr int kDecodeMaxRows = 8;    // the VALU split producer serves G*Sq <= 8
+constexpr int kDecodeMaxRows = 8;    // the VALU split producer handles G*Sq <= 8 ...
+constexpr int kDecodeValuRows = 4;   // ... and the split-KV paths give it G*Sq <= 4 (the MFMA
+                                     // producer streams faster with more rows)
 constexpr int kMaxGridYZ = 65535;
 
 struct Shape {
@@ -74,50 +76,69 @@ ef::KeyRuns key_runs(int Sq, int Skv, int window, int sinks) {
 // over the legal schedules, minimise the largest work/throughput ratio over
 // the modelled resources). Resources: HBM (K/V, q, o and the partial states
 // written and read back) and the streaming time of one workgroup (T keys of K
-// and V at a per-wave rate, times the rounds of workgroups the chip holds);
-// the combine follows (inside the producer for small P, else a second
-// kernel). The rates are measured on MI355X: 6.5 TB/s streaming reads (the
-// VALU decode producer), 5.0 TB/s for the MFMA producer, 8 and 5 GB/s per
-// wave, 2048 resident waves, about 3 us of fixed cost per workgroup round, 4
-// us for the combine inside the producer and 5 us plus its reads for the
-// combine kernel.
+// and V at that workgroup's rate, times the rounds of workgroups the chip
+// holds); the combine follows (inside the producer for up to 64 partitions,
+// else a second kernel). The rates were fitted to partition-size sweeps of
+// twelve decode shapes on MI355X (1 to 64 query rows per kv head, 1K to 128K
+// keys): the VALU producer streams 6.5 TB/s over the chip and 27.6, 51.1 or
+// 10.3 GB/s per workgroup for 1, 2 or 4 query rows per kv head (one, two and
+// one waves), plus 5 us per round; the combine inside it costs 4.4 us per 16
+// partitions, the combine kernel 8.9 us plus its reads. The MFMA producer
+// streams 5.85 TB/s over the chip and 9.9 GB/s per wave, plus 1 us per round,
+// and its combine kernel costs 13.4 us plus its reads. 2048 waves are resident.
+// The chip's rate is reached only with enough waves streaming at once: under
+// load a wave draws about 16 GB/s (VALU) or 8.5 GB/s (MFMA), counted over the
+// waves weighted by their share of the keys (a short last partition adds
+// little).
 constexpr double kHbmValuBytesPerUs = 6.5e6;
-constexpr double kHbmMfmaBytesPerUs = 5.0e6;
-constexpr double kWaveValuBytesPerUs = 8.0e3;
-constexpr double kWaveMfmaBytesPerUs = 5.0e3;
+constexpr double kHbmMfmaBytesPerUs = 5.85e6;
+constexpr double kWgValuBytesPerUs[3] = {27.6e3, 51.1e3, 10.3e3};  // 1, 2, 4 rows
+constexpr double kWaveMfmaBytesPerUs = 9.9e3;
+constexpr double kLoadedWaveValuBytesPerUs = 16.0e3;
+constexpr double kLoadedWaveMfmaBytesPerUs = 8.5e3;
 constexpr double kResidentWaves = 2048.0;
-constexpr double kRoundUs = 3.0;
-constexpr double kFusedCombineUs = 4.0;
-constexpr double kCombineLaunchUs = 5.0;
+constexpr double kRoundValuUs = 5.0;
+constexpr double kRoundMfmaUs = 1.0;
+constexpr double kFusedCombineUsPer16 = 4.4;
+constexpr double kCombineValuUs = 8.9;
+constexpr double kCombineMfmaUs = 13.4;
 
 double split_model_us(const Shape& s, int keys, int T) {
   const int G = s.Hq / s.Hkv;
   const int R = G * s.Sq;
   const double P = std::ceil((double)keys / T);
-  const bool valu = R <= kDecodeMaxRows;
-  double nw, wg_per_part;
+  const double Tk = std::min<double>(T, keys);
+  const bool valu = R <= kDecodeValuRows;
+  double nw, wg_per_part, wg_rate;
   if (valu) {
-    const int rmax = R <= 1 ? 1 : R <= 2 ? 2 : R <= 4 ? 4 : 8;
-    nw = (rmax == 1 || rmax == 4) ? 1 : 2;  // waves per workgroup of the VALU producer
+    const int bucket = R <= 1 ? 0 : R <= 2 ? 1 : 2;
+    nw = bucket == 1 ? 2 : 1;  // waves per workgroup of the VALU producer
     wg_per_part = 1;
+    wg_rate = kWgValuBytesPerUs[bucket];
   } else {
     const int bm = ef::mfma_rows_per_block(R);
     nw = bm / 32;
     wg_per_part = std::ceil((double)R / bm);
+    wg_rate = kWaveMfmaBytesPerUs * nw;
   }
   const double kv_heads = (double)s.B * s.Hkv;
   const double rows = (double)s.B * s.Hq * s.Sq;
   const double kv_bytes = kv_heads * keys * s.D * 4.0;
   const double io_bytes = rows * s.D * 6.0;
   const double state_bytes = rows * P * (s.D + 2) * 4.0;
-  const double r_hbm = (kv_bytes + io_bytes + 2.0 * state_bytes) /
-                       (valu ? kHbmValuBytesPerUs : kHbmMfmaBytesPerUs);
+  const double hbm = valu ? kHbmValuBytesPerUs : kHbmMfmaBytesPerUs;
   const double waves = kv_heads * P * wg_per_part * nw;
+  const double waves_eff = kv_heads * wg_per_part * nw * keys / Tk;
+  const double hbm_eff =
+      std::min(hbm, std::min(waves_eff, kResidentWaves) *
+                        (valu ? kLoadedWaveValuBytesPerUs : kLoadedWaveMfmaBytesPerUs));
+  const double r_hbm = (kv_bytes + io_bytes + 2.0 * state_bytes) / hbm_eff;
   const double rounds = std::ceil(waves / kResidentWaves);
-  const double wave_rate = valu ? kWaveValuBytesPerUs : kWaveMfmaBytesPerUs;
-  const double r_wg = rounds * ((double)T * s.D * 4.0 / (wave_rate * nw) + kRoundUs);
+  const double r_wg =
+      rounds * (Tk * s.D * 4.0 / wg_rate + (valu ? kRoundValuUs : kRoundMfmaUs));
   const bool fused = valu && P <= ef::kFusedMaxP;
-  const double combine = fused ? kFusedCombineUs : state_bytes / kHbmValuBytesPerUs + kCombineLaunchUs;
+  const double combine = fused ? kFusedCombineUsPer16 * std::ceil(P / 16.0)
+                               : state_bytes / hbm + (valu ? kCombineValuUs : kCombineMfmaUs);
   return std::max(r_hbm, r_wg) + combine;
 }
 
@@ -127,11 +148,10 @@ double split_model_us(const Shape& s, int keys, int T) {
 std::vector<int> partition_candidates(int keys) {
   std::vector<int> out;
   const long long top = ((long long)std::max(keys, 1) + kTileKeys - 1) / kTileKeys * kTileKeys;
-  for (long long t = kTileKeys; t < top; t *= 2) {
+  // Powers of two times the tile: sizes in between leave a ragged last
+  // partition on power-of-two contexts and measured slower than both neighbours.
+  for (long long t = kTileKeys; t < top; t *= 2)
     if ((keys + t - 1) / t <= kMaxGridYZ) out.push_back((int)t);
-    const long long t3 = t * 3 / 2;
-    if (t3 % kTileKeys == 0 && t3 < top && (keys + t3 - 1) / t3 <= kMaxGridYZ) out.push_back((int)t3);
-  }
   out.push_back((int)top);
   std::sort(out.begin(), out.end());
   out.erase(std::unique(out.begin(), out.end()), out.end());
@@ -222,6 +242,8 @@ const char* ef_status_string(int status) {
     case EF_ERR_HIP: return "HIP error while enqueueing work";
     case EF_ERR_INVALID_MASK: return "window must be >= 1 and sinks >= 0";
     case EF_ERR_INVALID_DIFF: return "lambda_init and eps must be finite and eps >= 0";
+    case EF_ERR_INVALID_SPLIT:
+      return "d_splits must be 1, 2 or 4, with at most 8 query rows per kv head";
     default: return "unknown status";
   }
 }
@@ -343,13 +365,15 @@ ef_status split_prepare(const Shape& s, const void* q, const void* k, const void
 
 // Stores the partition states; with `counters` and `o` given (decode path only),
 // the last workgroup of each (batch, kv head) also combines them into o.
+// d_splits = 0 lets the row count choose the producer; d_splits >= 1 asks for
+// the VALU producer with that many output-channel slices.
 ef_status split_produce(const Shape& s, const void* q, const void* k, const void* v, float scale,
                         int causal, const ef::KeyRuns& runs, int T, int P, float* ws_m,
                         float* ws_l, float* ws_acc, unsigned* counters, float* o,
-                        hipStream_t hs) {
+                        hipStream_t hs, int d_splits = 0) {
   const int G = s.Hq / s.Hkv;
   const int R = G * s.Sq;
-  if (R <= kDecodeMaxRows) {
+  if (d_splits > 0 || R <= kDecodeValuRows) {
     ef::DecodeParams a{};
     a.q = static_cast<const uint16_t*>(q);
     a.k = static_cast<const uint16_t*>(k);
@@ -367,6 +391,7 @@ ef_status split_produce(const Shape& s, const void* q, const void* k, const void
     a.counters = counters;
     a.o = o;
     a.runs = runs;
+    a.d_splits = d_splits > 0 ? d_splits : 1;
     return from_hip(ef::launch_decode_split(a, hs));
   }
   return launch_mfma(s, q, k, v, nullptr, ws_m, ws_l, ws_acc, T, P, scale, causal, runs, hs);
@@ -383,7 +408,7 @@ ef_status splitkv_impl(const Shape& s, const void* q, const void* k, const void*
   if (st != EF_OK || s.rows() == 0) return st;
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (s.Skv == 0) return from_hip(ef::launch_zero_fill(o, (size_t)s.rows() * s.D, hs));
-  const bool fused = (s.Hq / s.Hkv) * s.Sq <= kDecodeMaxRows && P <= ef::kFusedMaxP;
+  const bool fused = (s.Hq / s.Hkv) * s.Sq <= kDecodeValuRows && P <= ef::kFusedMaxP;
   if (fused)
     return split_produce(s, q, k, v, scale, causal, runs, T, P, ws_m, ws_l, ws_acc, counters, o,
                          hs);
@@ -640,6 +665,83 @@ size_t ef_diff_attention_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv,
   const long long P = diff_partitions(s, partition_size, &T);
   if (P <= 1) return 0;
   return ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv).bytes;
+}
+
+}  // extern "C"
+
+namespace {
+
+// Partitions of the output-channel split decode (1: no workspace), or 0 for an
+// invalid shape, partition size or split.
+long long dsplit_partitions(const Shape& s, int d_splits, int partition_size, int* T_out) {
+  if (check_shape(s) != EF_OK) return 0;
+  if (d_splits != 1 && d_splits != 2 && d_splits != 4) return 0;
+  if ((long long)(s.Hq / s.Hkv) * s.Sq > kDecodeMaxRows) return 0;
+  if (partition_size < 0 || partition_size % kTileKeys != 0) return 0;
+  if (s.rows() == 0 || s.Skv == 0) return 1;
+  const int T = resolve_partition(s, s.Skv, partition_size);
+  *T_out = T;
+  return (s.Skv + (long long)T - 1) / T;
+}
+
+}  // namespace
+
+extern "C" {
+
+ef_status ef_attention_decode_dsplit(const void* q, const void* k, const void* v, float* o, int B,
+                                     int Hq, int Hkv, int Sq, int Skv, int D, float scale,
+                                     int causal, int d_splits, int partition_size,
+                                     void* workspace, size_t workspace_bytes, void* stream) {
+  const Shape s{B, Hq, Hkv, Sq, Skv, D};
+  ef_status st = check_shape(s);
+  if (st != EF_OK) return st;
+  if (d_splits != 1 && d_splits != 2 && d_splits != 4) return EF_ERR_INVALID_SPLIT;
+  if ((long long)(Hq / Hkv) * Sq > kDecodeMaxRows) return EF_ERR_INVALID_SPLIT;
+  if (partition_size < 0 || partition_size % kTileKeys != 0) return EF_ERR_INVALID_PARTITION;
+  st = check_io(s, q, k, v, o, scale);
+  if (st != EF_OK) return st;
+  if (s.rows() == 0) return EF_OK;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  if (s.Skv == 0) return from_hip(ef::launch_zero_fill(o, (size_t)s.rows() * s.D, hs));
+  int T = 0;
+  const long long P = dsplit_partitions(s, d_splits, partition_size, &T);
+  if (P < 1 || P * d_splits > 0x7fffffffLL) return EF_ERR_INVALID_PARTITION;
+  const ef::KeyRuns runs = key_runs(Sq, Skv, 0, 0);
+  if (P == 1)  // each workgroup writes its channels of o: no workspace, no merge
+    return split_produce(s, q, k, v, scale, causal, runs, T, 1, nullptr, nullptr, nullptr,
+                         nullptr, o, hs, d_splits);
+  const WsLayout w = ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv * d_splits);
+  if (workspace == nullptr || workspace_bytes < w.bytes) return EF_ERR_WORKSPACE_TOO_SMALL;
+  if (misaligned(workspace)) return EF_ERR_MISALIGNED;
+  char* ws = static_cast<char*>(workspace);
+  float* ws_m = reinterpret_cast<float*>(ws + w.m_off);
+  float* ws_l = reinterpret_cast<float*>(ws + w.l_off);
+  float* ws_acc = reinterpret_cast<float*>(ws + w.acc_off);
+  unsigned* counters = reinterpret_cast<unsigned*>(ws + w.cnt_off);
+  if (P <= ef::kFusedMaxP)
+    return split_produce(s, q, k, v, scale, causal, runs, T, (int)P, ws_m, ws_l, ws_acc,
+                         counters, o, hs, d_splits);
+  st = split_produce(s, q, k, v, scale, causal, runs, T, (int)P, ws_m, ws_l, ws_acc, nullptr,
+                     nullptr, hs, d_splits);
+  if (st != EF_OK) return st;
+  ef::CombineParams c{};
+  c.m = ws_m;
+  c.l = ws_l;
+  c.acc = ws_acc;
+  c.o = o;
+  c.rows = (int)s.rows();
+  c.P = (int)P;
+  c.D = s.D;
+  return from_hip(ef::launch_combine(c, hs));
+}
+
+size_t ef_attention_decode_dsplit_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                                 int d_splits, int partition_size) {
+  const Shape s{B, Hq, Hkv, Sq, Skv, D};
+  int T = 0;
+  const long long P = dsplit_partitions(s, d_splits, partition_size, &T);
+  if (P <= 1) return 0;
+  return ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv * d_splits).bytes;
 }
 
 }  // extern "C"

@@ -29,6 +29,16 @@
 //    bf16 as the matrix-core kernel does; the sum l uses the fp32 weights.
 // Each row group carries its own rolling state; the groups of a wave and the
 // waves of the workgroup are merged with the same reducer at the end.
+//
+// Output-channel split (DS > 1; the N parallel refinement of the p.V product,
+// section 4.1 and table "rules", which the paper's evaluation selects for
+// one-sequence decode, section 7.2): DS
+// workgroups share a partition. Each reads the partition's whole K rows and
+// evaluates the same scores and softmax, but loads and accumulates only its
+// D/DS value channels and writes only those. The reference point and sum it
+// stores are bit-identical to the other slices' (same keys, same order), so
+// the combine of a slice needs only its own slice's workgroups. With one
+// partition and no workspace the workgroup writes o directly: no merge at all.
 #include "ef_device.hpp"
 #include "ef_kernels.hpp"
 #include "group_combine.hpp"
@@ -52,15 +62,17 @@ __device__ __forceinline__ uint32_t pair_hi(uint32_t a, uint32_t b) {
 
 }  // namespace
 
-// One partition p of the keys of kv head hkv of batch b, by the NW waves of the
-// calling workgroup.
-template <int D, int RMAX, int NW, int U, int CH, bool FUSED, bool LOCAL>
+// One partition p of the keys of kv head hkv of batch b, value channels
+// [ds * D/DS, (ds + 1) * D/DS), by the NW waves of the calling workgroup.
+template <int D, int RMAX, int NW, int U, int CH, bool FUSED, bool LOCAL, int DS>
 __device__ __forceinline__ void decode_partition(const DecodeParams& a, const int p, const int hkv,
-                                                 const int b) {
+                                                 const int b, const int ds) {
   constexpr int LPR = D / (8 * CH);  // lanes per key row
   constexpr int TPL = 64 / LPR;      // key rows per wave-wide load
   constexpr int DL = 8 * CH;         // value elements per lane and row
+  constexpr int DW = D / DS;         // value channels of this workgroup
   static_assert(U % 2 == 0, "keys are paired across the U slots");
+  static_assert(DW % 8 == 0, "a channel slice holds whole 16-byte chunks");
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int tl = lane / LPR;  // row slot inside a wave-wide load
@@ -84,6 +96,11 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& a, const in
       const_cast<uint16_t*>(a.v + (kvhead + rbase) * D), (short)0, (int)rbytes, kBufferFlags);
   // Query rows of this kv head are contiguous: row r = g*Sq + sq.
   const size_t row0 = ((size_t)b * a.Hq + (size_t)hkv * a.G) * (size_t)a.Sq;
+  // Value chunks of this lane inside the workgroup's channel slice; the others
+  // are read at the buffer's end (zero, no memory access).
+  bool vin[CH];
+#pragma unroll
+  for (int i = 0; i < CH; ++i) vin[i] = DS == 1 || ((dc + i * LPR) * 8) / DW == ds;
 
   // Positive scale: a negative one is moved into q. The floor keeps a zero
   // scale well defined (every visible key gets weight 1).
@@ -133,7 +150,8 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& a, const in
 #pragma unroll
       for (int i = 0; i < CH; ++i) {
         kr[u][i] = __builtin_amdgcn_raw_buffer_load_b128(krs, off + i * LPR * 16, 0, kNonTemporal);
-        vr[u][i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, off + i * LPR * 16, 0, kNonTemporal);
+        vr[u][i] = __builtin_amdgcn_raw_buffer_load_b128(vrs, vin[i] ? off + i * LPR * 16 : rbytes,
+                                                         0, kNonTemporal);
       }
     }
   };
@@ -287,8 +305,8 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& a, const in
   }
   __syncthreads();
   const int P = a.P;
-  for (int idx = threadIdx.x; idx < a.R * D; idx += NW * 64) {
-    const int r = idx / D, d = idx % D;
+  for (int idx = threadIdx.x; idx < a.R * DW; idx += NW * 64) {
+    const int r = idx / DW, d = ds * DW + idx % DW;
     float M = kNegInf;
 #pragma unroll
     for (int w = 0; w < NW; ++w) M = fmaxf(M, sm[w][r]);
@@ -302,15 +320,21 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& a, const in
     }
     const size_t slot = (row0 + r) * (size_t)P + p;
     const float mnat = (M == kNegInf) ? kNegInf : M * kLn2;  // natural-log units
-    if constexpr (FUSED) {
+    // Every channel slice stores the row's reference and sum (the same values):
+    // the combine of a slice waits only for that slice's workgroups.
+    const bool first = idx % DW == 0;
+    if (!FUSED && a.ws_acc == nullptr) {
+      // One partition, no workspace: the state is the row's result.
+      a.o[(row0 + r) * D + d] = (M == kNegInf || L == 0.f) ? 0.f : A / L;
+    } else if constexpr (FUSED) {
       store_dev(&a.ws_acc[slot * D + d], A);  // read by another workgroup in this launch
-      if (d == 0) {
+      if (first) {
         store_dev(&a.ws_m[slot], mnat);
         store_dev(&a.ws_l[slot], L);
       }
     } else {
       a.ws_acc[slot * D + d] = A;
-      if (d == 0) {
+      if (first) {
         a.ws_m[slot] = mnat;
         a.ws_l[slot] = L;
       }
@@ -323,16 +347,19 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& a, const in
     __shared__ float cw[RMAX * kFusedMaxP];
     __shared__ float cl[RMAX * kFusedMaxP];
     __shared__ float cinv[RMAX];
-    unsigned* counter = a.counters + ((size_t)b * a.Hkv + hkv) * kCounterStride;
+    unsigned* counter = a.counters + (((size_t)b * a.Hkv + hkv) * DS + ds) * kCounterStride;
     if (!last_of_group(counter, P)) return;
-    combine_group<D, NW * 64>(a.ws_m, a.ws_l, a.ws_acc, a.o, row0, a.R, P, cw, cl, cinv);
+    combine_group<D, DW, NW * 64>(a.ws_m, a.ws_l, a.ws_acc, a.o, row0, a.R, P, cw, cl, cinv,
+                                  ds * DW);
     if (threadIdx.x == 0) reset_counter(counter);
   }
 }
 
-template <int D, int RMAX, int NW, int U, int CH, bool FUSED, bool LOCAL>
+// Grid: x = partition * DS + channel slice, y = kv head, z = batch.
+template <int D, int RMAX, int NW, int U, int CH, bool FUSED, bool LOCAL, int DS>
 __global__ __launch_bounds__(NW * 64) void decode_split_kernel(DecodeParams a) {
-  decode_partition<D, RMAX, NW, U, CH, FUSED, LOCAL>(a, blockIdx.x, blockIdx.y, blockIdx.z);
+  decode_partition<D, RMAX, NW, U, CH, FUSED, LOCAL, DS>(a, blockIdx.x / DS, blockIdx.y,
+                                                          blockIdx.z, blockIdx.x % DS);
 }
 
 // Launch shape per row count, measured on one-token decode with 1024
@@ -345,16 +372,16 @@ constexpr int kWaves = (RMAX == 1 || RMAX == 4) ? 1 : 2;
 template <int RMAX>
 constexpr int kSlots = RMAX <= 2 ? 4 : 2;
 
-template <int D, int RMAX, bool LOCAL>
+template <int D, int RMAX, bool LOCAL, int DS>
 static hipError_t launch_decode_rl(const DecodeParams& a, hipStream_t stream) {
   constexpr int NW = kWaves<RMAX>;
   constexpr int U = kSlots<RMAX>;
-  dim3 grid(a.P, a.Hkv, a.B);
+  dim3 grid(a.P * DS, a.Hkv, a.B);
   if (a.counters != nullptr) {
-    hipLaunchKernelGGL((decode_split_kernel<D, RMAX, NW, U, 1, true, LOCAL>), grid, dim3(NW * 64),
-                       0, stream, a);
+    hipLaunchKernelGGL((decode_split_kernel<D, RMAX, NW, U, 1, true, LOCAL, DS>), grid,
+                       dim3(NW * 64), 0, stream, a);
   } else {
-    hipLaunchKernelGGL((decode_split_kernel<D, RMAX, NW, U, 1, false, LOCAL>), grid,
+    hipLaunchKernelGGL((decode_split_kernel<D, RMAX, NW, U, 1, false, LOCAL, DS>), grid,
                        dim3(NW * 64), 0, stream, a);
   }
   return hipGetLastError();
@@ -362,8 +389,12 @@ static hipError_t launch_decode_rl(const DecodeParams& a, hipStream_t stream) {
 
 template <int D, int RMAX>
 static hipError_t launch_decode_r(const DecodeParams& a, hipStream_t stream) {
-  return a.runs.window > 0 ? launch_decode_rl<D, RMAX, true>(a, stream)
-                           : launch_decode_rl<D, RMAX, false>(a, stream);
+  if (a.runs.window > 0) return launch_decode_rl<D, RMAX, true, 1>(a, stream);
+  switch (a.d_splits) {
+    case 2: return launch_decode_rl<D, RMAX, false, 2>(a, stream);
+    case 4: return launch_decode_rl<D, RMAX, false, 4>(a, stream);
+    default: return launch_decode_rl<D, RMAX, false, 1>(a, stream);
+  }
 }
 
 template <int D>

@@ -44,11 +44,13 @@ struct DecodeParams {
   int P;  // partitions
   float c;  // scale * log2(e)
   int causal;
-  // Fused combine (optional): per-(batch, kv head) arrival counters, zero on entry
-  // and left zero on exit, and the output o [B][Hq][Sq][D] fp32.
+  // Fused combine (optional): per-(batch, kv head, channel slice) arrival
+  // counters, zero on entry and left zero on exit, and the output o
+  // [B][Hq][Sq][D] fp32. With ws_acc null (one partition) o is written directly.
   unsigned* counters;
   float* o;
   KeyRuns runs;  // partitions cover the virtual key axis (T keys each)
+  int d_splits;  // output-channel slices per partition: 1 (0 also means 1), 2 or 4
 };
 
 // Largest partition count for which the producer combines its group itself.

@@ -52,20 +52,22 @@ __device__ __forceinline__ u32x4_t load16_dev(__amdgpu_buffer_rsrc_t rs, int off
   return __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, kDeviceScope);
 }
 
-// o[row0 + r][:] = sum_p exp(m_p - M) acc_p / sum_p exp(m_p - M) l_p over the
-// P stored states of rows row0 .. row0 + nrows - 1 (0 for a row with no
-// visible key), the states read with device-scope loads. cw, cl: LDS of at
-// least nrows * P floats; cinv: nrows floats. The combine is the tail of the
+// o[row0 + r][d0 : d0 + DW] = sum_p exp(m_p - M) acc_p / sum_p exp(m_p - M) l_p
+// over the P stored states of rows row0 .. row0 + nrows - 1 (0 for a row with
+// no visible key), the states read with device-scope loads; DW = D unless the
+// group covers one output-channel slice of the rows. cw, cl: LDS of at least
+// nrows * P floats; cinv: nrows floats. The combine is the tail of the
 // producer that arrives last, so it is arranged for few round trips: each
 // thread owns two 4-element slices of the output rows and requests the value
 // states of 16 partitions of both at once, the first 16 together with the
 // reference points and sums.
-template <int D, int NT>
+template <int D, int DW, int NT>
 __device__ __forceinline__ void combine_group(const float* ws_m, const float* ws_l,
                                               const float* ws_acc, float* o, size_t row0,
                                               int nrows, int P, float* cw, float* cl,
-                                              float* cinv) {
-  constexpr int D4 = D / 4;  // 4-element slices of a row
+                                              float* cinv, int d0) {
+  static_assert(DW % 4 == 0 && D % DW == 0, "whole 4-element slices of a row");
+  constexpr int D4 = DW / 4;  // 4-element slices of a row's channel range
   constexpr int BATCH = 16;  // partitions per slice in flight
   const int n = nrows * P;
   const int bytes = n * D * 4;  // at most 8 * 64 * 128 * 4
@@ -76,7 +78,7 @@ __device__ __forceinline__ void combine_group(const float* ws_m, const float* ws
   // Byte offset of slice c's value state in partition p; the buffer's end (a
   // zero read) past the row's partitions or past the slices.
   auto slice_off = [&](int c, int p) {
-    return (c < nslices && p < P) ? ((c / D4) * P * D + p * D + (c % D4) * 4) * 4 : bytes;
+    return (c < nslices && p < P) ? ((c / D4) * P * D + p * D + d0 + (c % D4) * 4) * 4 : bytes;
   };
   auto load_batch = [&](int c0, int p0, u32x4_t (&x0)[BATCH], u32x4_t (&x1)[BATCH]) {
 #pragma unroll
@@ -103,7 +105,7 @@ __device__ __forceinline__ void combine_group(const float* ws_m, const float* ws
   auto store_slice = [&](int c, const floatx4& sv) {
     if (c < nslices) {
       const float inv = cinv[c / D4];
-      *reinterpret_cast<float4*>(o + (row0 + c / D4) * D + (c % D4) * 4) =
+      *reinterpret_cast<float4*>(o + (row0 + c / D4) * D + d0 + (c % D4) * 4) =
           make_float4(sv[0] * inv, sv[1] * inv, sv[2] * inv, sv[3] * inv);
     }
   };

@@ -31,6 +31,7 @@ STATUS_NAMES = {
     9: "EF_ERR_HIP",
     10: "EF_ERR_INVALID_MASK",
     11: "EF_ERR_INVALID_DIFF",
+    12: "EF_ERR_INVALID_SPLIT",
 }
 
 # Exported symbols and their C signatures (restype, argtypes).
@@ -57,6 +58,9 @@ SIGNATURES = {
     "ef_diff_attention": (_i, [_vp, _vp, _vp, _vp, _vp, _fp, _fp, _fp, _fp, _fp, _fp, _f, _f, _i,
                                _i, _i, _i, _i, _i, _f, _i, _i, _vp, _sz, _vp]),
     "ef_diff_attention_workspace_size": (_sz, [_i, _i, _i, _i, _i, _i, _i]),
+    "ef_attention_decode_dsplit": (_i, [_vp, _vp, _vp, _fp, _i, _i, _i, _i, _i, _i, _f, _i, _i,
+                                        _i, _vp, _sz, _vp]),
+    "ef_attention_decode_dsplit_workspace_size": (_sz, [_i, _i, _i, _i, _i, _i, _i, _i]),
 }
 
 
@@ -129,6 +133,19 @@ def ef_diff_attention(q1, q2, k1, k2, v, o, lambda_q1, lambda_k1, lambda_q2, lam
 
 def ef_diff_attention_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size) -> int:
     return _lib().ef_diff_attention_workspace_size(B, Hq, Hkv, Sq, Skv, D, partition_size)
+
+
+def ef_attention_decode_dsplit(q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale, causal, d_splits,
+                               partition_size, workspace, workspace_bytes, stream) -> int:
+    return _lib().ef_attention_decode_dsplit(q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale,
+                                             int(causal), d_splits, partition_size, workspace,
+                                             workspace_bytes, stream)
+
+
+def ef_attention_decode_dsplit_workspace_size(B, Hq, Hkv, Sq, Skv, D, d_splits,
+                                              partition_size) -> int:
+    return _lib().ef_attention_decode_dsplit_workspace_size(B, Hq, Hkv, Sq, Skv, D, d_splits,
+                                                            partition_size)
 
 
 def ef_attention_combine(m, l, acc, o, rows, num_partitions, D, stream) -> int:
@@ -459,4 +476,31 @@ def diff_attention(q1, q2, k1, k2, v, lambda_q1, lambda_k1, lambda_q2, lambda_k2
                            float(lambda_init), float(eps), B, Hq, Hkv, Sq, Skv, D, float(scale),
                            causal, partition_size, ws_ptr, ws_bytes, _stream_handle(stream))
     _check(st, "ef_diff_attention")
+    return o
+
+
+def attention_decode_dsplit(q, k, v, scale: Optional[float] = None, causal: bool = False,
+                            d_splits: int = 2, partition_size: int = 0, workspace=None, out=None,
+                            stream=None):
+    """Decode through ef_attention_decode_dsplit: d_splits workgroups per key partition, each
+    writing D/d_splits output channels. With one partition (partition_size >= Skv) no workspace
+    is used and nothing is merged. A workspace made here is zero-filled (arrival counters)."""
+    torch = _torch()
+    B, Hq, Hkv, Sq, Skv, D = _check_qkv(q, k, v)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    o = _out(q, out)
+    need = int(ef_attention_decode_dsplit_workspace_size(B, Hq, Hkv, Sq, Skv, D, d_splits,
+                                                         partition_size))
+    if workspace is None and need > 0:
+        workspace = torch.zeros(need, dtype=torch.uint8, device=q.device)
+    if workspace is not None:
+        _check_workspace(workspace, q)
+        ws_ptr, ws_bytes = workspace.data_ptr(), workspace.numel() * workspace.element_size()
+    else:
+        ws_ptr, ws_bytes = None, 0
+    st = ef_attention_decode_dsplit(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B, Hq,
+                                    Hkv, Sq, Skv, D, float(scale), causal, d_splits,
+                                    partition_size, ws_ptr, ws_bytes, _stream_handle(stream))
+    _check(st, "ef_attention_decode_dsplit")
     return o

@@ -44,6 +44,7 @@ class AttentionConfig:
     window: int = 0  # local attention: keys j > n_i - window are visible (causal only)
     sinks: int = 0   # ... and keys j < sinks
     diff: bool = False  # differential attention: two q/k branches over one v
+    d_splits: int = 0   # > 0: decode through the output-channel split, this many slices
 
     @property
     def local(self) -> bool:
@@ -145,7 +146,15 @@ DIFF_CONFIGS: Tuple[AttentionConfig, ...] = (
                     causal=True, diff=True),
 )
 
-ALL_CONFIGS: Tuple[AttentionConfig, ...] = CONFIGS + LOCAL_CONFIGS + DIFF_CONFIGS
+# One-sequence MHA decode (section 7.2: at B = 1 the paper's selected kernel
+# splits each head's output channels over two blocks and needs no merge):
+# Llama 2 7B shape at a 4096-token context, one partition, two slices.
+DSPLIT_CONFIGS: Tuple[AttentionConfig, ...] = (
+    AttentionConfig("mha_decode_b1_h32_kv4096_d128", 1, 32, 32, 1, 4096, 128, causal=False,
+                    partition_size=4096, d_splits=2),
+)
+
+ALL_CONFIGS: Tuple[AttentionConfig, ...] = CONFIGS + LOCAL_CONFIGS + DIFF_CONFIGS + DSPLIT_CONFIGS
 
 CONFIG_BY_NAME: Dict[str, AttentionConfig] = {c.name: c for c in ALL_CONFIGS}
 

@@ -54,7 +54,7 @@ def test_library_exports_every_header_symbol():
 @needs_lib
 def test_status_strings():
     lib = ef.library()
-    for s in range(0, 12):
+    for s in range(0, 13):
         assert lib.ef_status_string(s)
         assert lib.ef_status_string(s) != b"unknown status"
     assert lib.ef_status_string(0) == b"ok"
@@ -107,9 +107,19 @@ def diff(**kw):
                                 a["causal"], a["T"], a["ws"], a["wsb"], a["stream"])
 
 
+def dsplit(**kw):
+    a = dict(q=A, k=A, v=A, o=A, B=1, Hq=4, Hkv=2, Sq=1, Skv=1000, D=128, scale=0.1, causal=0,
+             DS=2, T=256, ws=A, wsb=1 << 30, stream=None)
+    a.update(kw)
+    return ef.ef_attention_decode_dsplit(a["q"], a["k"], a["v"], a["o"], a["B"], a["Hq"],
+                                         a["Hkv"], a["Sq"], a["Skv"], a["D"], a["scale"],
+                                         a["causal"], a["DS"], a["T"], a["ws"], a["wsb"],
+                                         a["stream"])
+
+
 @needs_lib
-@pytest.mark.parametrize("call", [fwd, split, fwd_local, split_local, diff],
-                         ids=["fwd", "splitkv", "fwd_local", "splitkv_local", "diff"])
+@pytest.mark.parametrize("call", [fwd, split, fwd_local, split_local, diff, dsplit],
+                         ids=["fwd", "splitkv", "fwd_local", "splitkv_local", "diff", "dsplit"])
 def test_validation_errors(call):
     assert call(D=96) == 4
     assert call(D=0) == 4
@@ -194,6 +204,28 @@ def test_diff_specific_validation():
     assert ef.ef_diff_attention_workspace_size(1, 4, 2, 8, 1000, 128, 100) == 0
     # Nothing to compute: accepted, the lambda vectors are not needed.
     assert diff(B=0, lq1=None, gamma=None) == 0
+
+
+@needs_lib
+def test_dsplit_specific_validation():
+    for bad in (0, 3, 8, -2):
+        assert dsplit(DS=bad) == 12
+    assert dsplit(Hq=32, Hkv=2) == 12      # 16 query rows per kv head
+    assert dsplit(Sq=3, Hq=6, Hkv=2) == 12  # 9 rows
+    assert dsplit(T=100) == 6
+    assert dsplit(ws=None) == 7
+    sz = ef.ef_attention_decode_dsplit_workspace_size
+    need = sz(1, 4, 2, 1, 1000, 128, 2, 256)
+    # The split-KV layout with B*Hkv*d_splits counter slots.
+    assert need == ef.ef_attention_splitkv_workspace_size(1, 4, 2, 1, 1000, 128, 256) + 2 * 256
+    assert sz(1, 4, 2, 1, 1000, 128, 4, 256) == need + 4 * 256
+    assert dsplit(wsb=need - 1) == 7
+    assert dsplit(ws=MIS, wsb=need) == 5
+    # One partition: no workspace.
+    assert sz(1, 4, 2, 1, 1000, 128, 2, 1024) == 0
+    assert sz(1, 4, 2, 1, 1000, 128, 3, 256) == 0
+    assert sz(1, 32, 2, 1, 1000, 128, 2, 256) == 0
+    assert dsplit(B=0, q=None, o=None) == 0
 
 
 @needs_lib
@@ -283,20 +315,28 @@ def test_local_workspace_and_partition_arithmetic():
 
 @needs_lib
 def test_roofline_partition_choice():
-    """partition_size = 0 takes the candidate the roofline model rates fastest; on MI355X the
-    model's picks are the measured best of {256, ..., 4096} for these three decodes."""
+    """partition_size = 0 takes the candidate the roofline model rates fastest. On MI355X the
+    picks below were the measured best of 64, 128, ..., 8192 keys per partition (or within 3%
+    of it: the (2, 32, 8, 1, 2048) decode runs 16.0 us at 128 keys and 15.6 us at 64)."""
     ps = ef.ef_attention_splitkv_partition_size
     model = ef.ef_attention_splitkv_modeled_us
     assert ps(8, 32, 8, 1, 4096, 128, 0) == 256        # GQA decode: 16 partitions, fused combine
     assert ps(1, 32, 8, 1, 131072, 128, 0) == 1024     # 131072-key decode
     assert ps(16, 64, 8, 8, 8192, 128, 0) == 2048      # chunked decode (MFMA producer)
+    assert ps(1, 32, 32, 1, 4096, 128, 0) == 256       # one-sequence MHA decode
+    assert ps(1, 32, 32, 1, 16384, 128, 0) == 1024
+    assert ps(4, 64, 8, 1, 8192, 128, 0) == 512        # 8 rows per kv head: MFMA producer
+    assert ps(8, 32, 16, 1, 4096, 128, 0) == 2048      # 2 rows per kv head
+    assert ps(2, 32, 8, 1, 2048, 128, 0) == 128
+    # sink decode (4 sinks + 4096-key window of 32768): 2048 keys, 89 us vs 121 us at 64
+    assert ef.ef_attention_splitkv_local_partition_size(8, 32, 32, 1, 32768, 128, 4096, 4, 0) == 2048
     for shape in [(8, 32, 8, 1, 4096, 128), (1, 32, 8, 1, 131072, 128), (16, 64, 8, 8, 8192, 128),
                   (2, 8, 2, 3, 900, 128), (1, 4, 4, 1, 70, 64)]:
         t = ps(*shape, 0)
         assert t > 0 and t % 64 == 0
         best = model(*shape, 0, 0, t)
         assert best > 0
-        for cand in (64, 128, 192, 256, 384, 512, 768, 1024, 2048, 4096):
+        for cand in (64, 128, 256, 512, 1024, 2048, 4096):
             if cand <= -(-shape[4] // 64) * 64:
                 assert model(*shape, 0, 0, cand) >= best - 1e-9, (shape, cand)
     # the model: more partitions cost combine traffic, fewer cost per-workgroup streaming time
