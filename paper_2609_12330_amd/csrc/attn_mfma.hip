@@ -243,18 +243,19 @@ struct Tile {
   }
 
   // Weights 2^(x*c - reference) as bf16 pairs (P^T fragments) and their row
-  // sum, taken over the rounded weights the value product uses (one packed
-  // dot product with (1, 1) per pair).
+  // sum in fp32. (A packed bf16 dot product with (1, 1) per pair would sum the
+  // rounded weights in half the instructions, but between matrix products it
+  // costs about ten cycles each; the two sums differ by far less than the
+  // rounding of the weights themselves.)
   static __device__ __forceinline__ void weights(const floatx16* x, float c, float mneg,
                                                  uint32_t* pk, float& lsum) {
-    constexpr uint32_t kOnes = 0x3f803f80u;  // bf16 pair (1, 1)
     float ps[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const float p0 = exp2_fast(fmaf(x[(2 * i) >> 4][(2 * i) & 15], c, mneg));
       const float p1 = exp2_fast(fmaf(x[(2 * i + 1) >> 4][(2 * i + 1) & 15], c, mneg));
       pk[i] = pack_bf16x2(p0, p1);
-      ps[i & 3] = dot2_bf16(pk[i], kOnes, ps[i & 3]);
+      ps[i & 3] += p0 + p1;
     }
     lsum += (ps[0] + ps[1]) + (ps[2] + ps[3]);
   }

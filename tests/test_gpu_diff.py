@@ -23,6 +23,11 @@ pytestmark = pytest.mark.gpu
 
 MAX_ABS = 1e-2
 MEAN_ABS = 1e-3
+# The layer's output is normalised to RMS |1 - lambda_init| * |gamma| per row, so
+# its absolute error is the relative error of y = A1 - lambda * A2 times that
+# scale. The bars above are taken at the layer's own lambda_init = 0.8 (scale
+# 0.2); for another lambda_init they scale by |1 - lambda_init| / 0.2.
+LAMBDA_INIT_REF = 0.8
 
 
 def announce(msg):
@@ -43,12 +48,13 @@ def f64(t):
     return t.detach().cpu().double().numpy()
 
 
-def assert_close(o, ref, what):
+def assert_close(o, ref, what, lambda_init=LAMBDA_INIT_REF):
     o = o.detach().cpu().double().numpy() if isinstance(o, torch.Tensor) else o
     assert np.isfinite(o).all(), f"{what}: non-finite output"
     d = np.abs(o - ref)
     mx, mean = float(d.max()) if d.size else 0.0, float(d.mean()) if d.size else 0.0
-    assert mx <= MAX_ABS and mean <= MEAN_ABS, f"{what}: max {mx:.3e} mean {mean:.3e}"
+    f = max(1.0, abs(1.0 - lambda_init) / abs(1.0 - LAMBDA_INIT_REF))
+    assert mx <= MAX_ABS * f and mean <= MEAN_ABS * f, f"{what}: max {mx:.3e} mean {mean:.3e}"
 
 
 def run_gpu(inp, lambda_init, eps, scale, causal, partition_size=0, workspace=None, out=None):
@@ -96,7 +102,8 @@ def test_diff_negative_scale_and_other_lambda():
     for T in (1024, 64):
         o = run_gpu(inp, 0.3, 1e-6, -0.09, True, T)
         torch.cuda.synchronize()
-        assert_close(o, run_oracle(inp, 0.3, 1e-6, -0.09, True), f"negative scale T={T}")
+        assert_close(o, run_oracle(inp, 0.3, 1e-6, -0.09, True), f"negative scale T={T}",
+                     lambda_init=0.3)
 
 
 def test_diff_zero_rows_with_zero_eps():
