@@ -109,14 +109,14 @@ def cpu_baseline(cfg, inputs, budget_s, unit_fn):
                                  sinks=cfg.sinks)
 
     run()  # warm caches and pools
+    reps = 0
     t0 = time.perf_counter()
-    run()
-    one = max(time.perf_counter() - t0, 1e-6)
-    reps = max(1, int(budget_s / one))
-    t0 = time.perf_counter()
-    for _ in range(reps):
+    while True:  # whole passes until the budget is spent
         run()
-    dt = time.perf_counter() - t0
+        reps += 1
+        dt = time.perf_counter() - t0
+        if dt >= budget_s:
+            break
     value = unit_fn(reps * frac) / dt  # the work of `reps` samples of the workload per second
     return {
         "value": round(value, 4),
