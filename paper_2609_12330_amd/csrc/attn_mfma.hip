@@ -124,14 +124,16 @@ struct Loader {
   using G = TileGeom<D>;
   static constexpr int INSTS = BN / G::RPI / NW;  // direct loads per wave and tile
   static_assert(INSTS * G::RPI * NW == BN, "tile split over the waves");
-  int row[INSTS];     // tile row whose chunk this lane loads
-  int kchunk[INSTS];  // element offset of that chunk in a K row
-  int vchunk[INSTS];  // element offset of that chunk in a V row
-  int wave;
+  int row[INSTS];       // tile row whose chunk this lane loads
+  int kchunk[INSTS];    // element offset of that chunk in a K row
+  int vchunk[INSTS];    // element offset of that chunk in a V row
+  unsigned koff[INSTS];  // byte offset of this lane's K chunk from the tile's first row
+  unsigned voff[INSTS];  // the same for V
+  int wave;              // wave index, uniform (scalar)
 
   __device__ __forceinline__ void init() {
     const int lane = threadIdx.x & 63;
-    wave = threadIdx.x >> 6;
+    wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
     for (int i = 0; i < INSTS; ++i) {
       const int blk = wave + NW * i;
@@ -139,19 +141,34 @@ struct Loader {
       const int slot = lane % G::KCH;
       kchunk[i] = (slot ^ G::swz_k(row[i])) * 8;
       vchunk[i] = (slot ^ G::swz_v(row[i])) * 8;
+      koff[i] = (unsigned)(row[i] * D + kchunk[i]) * 2u;
+      voff[i] = (unsigned)(row[i] * D + vchunk[i]) * 2u;
     }
   }
 
+  // The address is a uniform base (the tile's first row) plus a 32-bit lane
+  // offset, so the vector ALU only clamps rows of a ragged tile.
   template <bool ISK>
   __device__ __forceinline__ void load(char* stage, const uint16_t* head, int kb, int kend) const {
     const int nrows = kend - kb;
     if (nrows <= 0) return;
+    const char* base = reinterpret_cast<const char*>(head + (size_t)kb * D);
+    if (nrows >= BN) {
 #pragma unroll
-    for (int i = 0; i < INSTS; ++i) {
-      const int r = min(row[i], nrows - 1);
-      const uint16_t* g = head + (size_t)(kb + r) * D + (ISK ? kchunk[i] : vchunk[i]);
-      char* l = stage + (wave + NW * i) * 1024;
-      __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)l, 16, 0, 0);
+      for (int i = 0; i < INSTS; ++i) {
+        char* l = stage + (wave + NW * i) * 1024;
+        const uint16_t* g = reinterpret_cast<const uint16_t*>(base + (ISK ? koff[i] : voff[i]));
+        __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)l, 16, 0, 0);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < INSTS; ++i) {
+        const int r = min(row[i], nrows - 1);
+        const unsigned off = (unsigned)(r * D + (ISK ? kchunk[i] : vchunk[i])) * 2u;
+        char* l = stage + (wave + NW * i) * 1024;
+        const uint16_t* g = reinterpret_cast<const uint16_t*>(base + off);
+        __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)l, 16, 0, 0);
+      }
     }
   }
   template <int S>
