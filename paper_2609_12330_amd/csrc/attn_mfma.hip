@@ -232,13 +232,32 @@ struct Tile {
         for (int i = 0; i < 16; ++i) x[half][i] = -x[half][i];
     }
     if (masked) {
+      // Element i of half `half` holds key base + o(i) with a compile-time offset o.
+      // The hidden keys become per-lane offset thresholds, clamped to the tile so the
+      // arithmetic cannot overflow: past `vis` (the run's end or the causal limit), and
+      // inside [wlo, whi] (left of the window, not a sink). Selects, not branches.
+      const int base = kb + 4 * h;
+      const int vis = min(min(kend - 1, lim), kb + BN) - base;
+      const int wlo = max(sinks, kb) - base;
+      const int whi = min(max(lo, kb - 1), kb + BN) - base;
+      if (__builtin_amdgcn_ballot_w64(whi >= wlo)) {
 #pragma unroll
-      for (int half = 0; half < 2; ++half)
+        for (int half = 0; half < 2; ++half)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int key = kb + half * 32 + 8 * (i >> 2) + 4 * h + (i & 3);
-          if (key >= kend || key > lim || (key <= lo && key >= sinks)) x[half][i] = kNegInf;
-        }
+          for (int i = 0; i < 16; ++i) {
+            const int o = half * 32 + 8 * (i >> 2) + (i & 3);
+            const bool hide = (o > vis) | ((o >= wlo) & (o <= whi));
+            x[half][i] = hide ? kNegInf : x[half][i];
+          }
+      } else {
+#pragma unroll
+        for (int half = 0; half < 2; ++half)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int o = half * 32 + 8 * (i >> 2) + (i & 3);
+            x[half][i] = o > vis ? kNegInf : x[half][i];
+          }
+      }
     }
     float tmax = fmaxf(x[0][0], x[0][1]);
 #pragma unroll
