@@ -16,6 +16,7 @@
 #pragma once
 
 #include "ef_device.hpp"
+#include "ef_kernels.hpp"
 
 namespace ef {
 
@@ -55,13 +56,13 @@ __device__ __forceinline__ u32x4_t load16_dev(__amdgpu_buffer_rsrc_t rs, int off
 // o[row0 + r][d0 : d0 + DW] = sum_p exp(m_p - M) acc_p / sum_p exp(m_p - M) l_p
 // over the P stored states of rows row0 .. row0 + nrows - 1 (0 for a row with
 // no visible key), the states read with device-scope loads; DW = D unless the
-// group covers one output-channel slice of the rows. cw, cl: LDS of at least
-// nrows * P floats; cinv: nrows floats. The combine is the tail of the
-// producer that arrives last, so it is arranged for few round trips: each
-// thread owns two 4-element slices of the output rows and requests the value
-// states of 16 partitions of both at once, the first 16 together with the
-// reference points and sums.
-template <int D, int DW, int NT>
+// group covers one output-channel slice of the rows; nrows <= MAXROWS and
+// P <= kFusedMaxP. cw, cl: LDS of at least nrows * P floats; cinv: nrows
+// floats. The combine is the tail of the producer that arrives last, so it is
+// arranged for few round trips: each thread owns two 4-element slices of the
+// output rows and requests the value states of 16 partitions of both at once,
+// the first 16 right behind the reference points and sums.
+template <int D, int DW, int NT, int MAXROWS>
 __device__ __forceinline__ void combine_group(const float* ws_m, const float* ws_l,
                                               const float* ws_acc, float* o, size_t row0,
                                               int nrows, int P, float* cw, float* cl,
@@ -93,8 +94,11 @@ __device__ __forceinline__ void combine_group(const float* ws_m, const float* ws
 #pragma unroll
     for (int j = 0; j < BATCH; ++j) {
       const int p = min(p0 + j, P - 1);
-      const float w0 = p0 + j < P ? cw[r0 * P + p] : 0.f;
-      const float w1 = p0 + j < P ? cw[r1 * P + p] : 0.f;
+      // Unconditional reads of a clamped index (a guarded read compiles to a branch
+      // per partition); a weight past the row's partitions counts zero times.
+      const float in = p0 + j < P ? 1.f : 0.f;
+      const float w0 = cw[r0 * P + p] * in;
+      const float w1 = cw[r1 * P + p] * in;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         s0[e] = fmaf(w0, __uint_as_float(x0[j][e]), s0[e]);
@@ -110,12 +114,29 @@ __device__ __forceinline__ void combine_group(const float* ws_m, const float* ws
     }
   };
 
+  // The reference points and sums first, all requested before any is used, then
+  // the first values: loads complete in order, so the barrier waits for the
+  // small loads only and the values land while the weights are formed.
+  // At most MAXROWS rows of at most kFusedMaxP partitions: KMAX states per thread.
+  constexpr int KMAX = (MAXROWS * kFusedMaxP + NT - 1) / NT;
+  float mv[KMAX], lv[KMAX];
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) {
+    if (k * NT < n) {
+      const int i = min((int)threadIdx.x + k * NT, n - 1);
+      mv[k] = load_dev(ws_m + row0 * P + i);
+      lv[k] = load_dev(ws_l + row0 * P + i);
+    }
+  }
   u32x4_t x0[BATCH], x1[BATCH];
-  load_batch(threadIdx.x, 0, x0, x1);  // first values in flight with the m, l reads
-#pragma unroll 8
-  for (int i = threadIdx.x; i < n; i += NT) {
-    cw[i] = load_dev(ws_m + row0 * P + i);
-    cl[i] = load_dev(ws_l + row0 * P + i);
+  load_batch(threadIdx.x, 0, x0, x1);
+#pragma unroll
+  for (int k = 0; k < KMAX; ++k) {
+    const int i = (int)threadIdx.x + k * NT;
+    if (k * NT < n && i < n) {
+      cw[i] = mv[k];
+      cl[i] = lv[k];
+    }
   }
   __syncthreads();
   for (int r = threadIdx.x; r < nrows; r += NT) {
