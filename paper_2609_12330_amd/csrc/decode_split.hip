@@ -50,6 +50,7 @@ namespace {
 constexpr float kMoveThreshold = 8.f;  // base-2 headroom before the reference moves
 constexpr uint32_t kBufferFlags = 0x00020000u;  // raw 32-bit buffer access
 constexpr int kNonTemporal = 2;                 // cache policy of streamed loads
+constexpr int kDeviceScopeStore = 16;           // cache policy sc1: device-coherent store
 
 // Pairs (x of key a, x of key b) of the bf16 elements 2w (lo) and 2w+1 (hi) of
 // two packed words, for a packed-bf16 dot product over the two keys.
@@ -287,56 +288,119 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& a, const in
   merge_groups(std::integral_constant<int, 4 * LPR>{});
   merge_groups(std::integral_constant<int, 8 * LPR>{});
 
-  // Merge the waves through LDS and store the partition's state.
-  __shared__ float sm[NW][RMAX], sl[NW][RMAX];
-  __shared__ float sacc[NW][RMAX][D];
-  if (tl == 0) {
-#pragma unroll
-    for (int r = 0; r < RMAX; ++r) {
-      if (dc == 0) {
-        sm[wave][r] = m[r];
-        sl[wave][r] = l[r];
-      }
-#pragma unroll
-      for (int i = 0; i < CH; ++i)
-#pragma unroll
-        for (int e = 0; e < 8; ++e) sacc[wave][r][(dc + i * LPR) * 8 + e] = acc[r][i * 8 + e];
-    }
-  }
-  __syncthreads();
   const int P = a.P;
-  for (int idx = threadIdx.x; idx < a.R * DW; idx += NW * 64) {
-    const int r = idx / DW, d = ds * DW + idx % DW;
-    float M = kNegInf;
+  if constexpr (NW == 1) {
+    // One wave: the lanes of row group 0 hold the partition's merged state (the
+    // merge across waves below would weight it by exactly 1), so they store it
+    // straight from registers, 16 bytes at a time; no LDS round trip, no barrier.
+    if (tl == 0) {
 #pragma unroll
-    for (int w = 0; w < NW; ++w) M = fmaxf(M, sm[w][r]);
-    const float ms = (M == kNegInf) ? 0.f : M;
-    float L = 0.f, A = 0.f;
+      for (int r = 0; r < RMAX; ++r) {
+        if (r >= a.R) break;
+        const float M = m[r], L = l[r];
+        const size_t slot = (row0 + r) * (size_t)P + p;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) {
-      const float wt = exp2_fast(sm[w][r] - ms);
-      L = fmaf(wt, sl[w][r], L);
-      A = fmaf(wt, sacc[w][r][d], A);
-    }
-    const size_t slot = (row0 + r) * (size_t)P + p;
-    const float mnat = (M == kNegInf) ? kNegInf : M * kLn2;  // natural-log units
-    // Every channel slice stores the row's reference and sum (the same values):
-    // the combine of a slice waits only for that slice's workgroups.
-    const bool first = idx % DW == 0;
-    if (!FUSED && a.ws_acc == nullptr) {
-      // One partition, no workspace: the state is the row's result.
-      a.o[(row0 + r) * D + d] = (M == kNegInf || L == 0.f) ? 0.f : A / L;
-    } else if constexpr (FUSED) {
-      store_dev(&a.ws_acc[slot * D + d], A);  // read by another workgroup in this launch
-      if (first) {
-        store_dev(&a.ws_m[slot], mnat);
-        store_dev(&a.ws_l[slot], L);
+        for (int i = 0; i < CH; ++i) {
+          if (!vin[i]) continue;
+          const int d = (dc + i * LPR) * 8;  // first of this lane's 8 value channels
+          const float* x = &acc[r][i * 8];
+          if (!FUSED && a.ws_acc == nullptr) {
+            // One partition, no workspace: the state is the row's result.
+            const bool none = M == kNegInf || L == 0.f;
+            float* op = a.o + (row0 + r) * D + d;
+            *reinterpret_cast<float4*>(op) =
+                none ? make_float4(0.f, 0.f, 0.f, 0.f)
+                     : make_float4(x[0] / L, x[1] / L, x[2] / L, x[3] / L);
+            *reinterpret_cast<float4*>(op + 4) =
+                none ? make_float4(0.f, 0.f, 0.f, 0.f)
+                     : make_float4(x[4] / L, x[5] / L, x[6] / L, x[7] / L);
+            continue;
+          }
+          const float mnat = (M == kNegInf) ? kNegInf : M * kLn2;  // natural-log units
+          // Every channel slice stores the row's reference and sum (the same values):
+          // the combine of a slice waits only for that slice's workgroups.
+          const bool first = d == ds * DW;
+          if constexpr (FUSED) {
+            // Read by another workgroup in this launch: device-scope stores into
+            // the group's block of value states (at most 8 rows x 64 partitions).
+            const __amdgpu_buffer_rsrc_t wrs = __builtin_amdgcn_make_buffer_rsrc(
+                a.ws_acc + row0 * (size_t)P * D, (short)0, a.R * P * D * 4, kBufferFlags);
+            const int off = ((r * P + p) * D + d) * 4;
+            __builtin_amdgcn_raw_buffer_store_b128(
+                u32x4_t{__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]),
+                        __float_as_uint(x[3])},
+                wrs, off, 0, kDeviceScopeStore);
+            __builtin_amdgcn_raw_buffer_store_b128(
+                u32x4_t{__float_as_uint(x[4]), __float_as_uint(x[5]), __float_as_uint(x[6]),
+                        __float_as_uint(x[7])},
+                wrs, off + 16, 0, kDeviceScopeStore);
+            if (first) {
+              store_dev(&a.ws_m[slot], mnat);
+              store_dev(&a.ws_l[slot], L);
+            }
+          } else {
+            float* ap = a.ws_acc + slot * D + d;
+            *reinterpret_cast<float4*>(ap) = make_float4(x[0], x[1], x[2], x[3]);
+            *reinterpret_cast<float4*>(ap + 4) = make_float4(x[4], x[5], x[6], x[7]);
+            if (first) {
+              a.ws_m[slot] = mnat;
+              a.ws_l[slot] = L;
+            }
+          }
+        }
       }
-    } else {
-      a.ws_acc[slot * D + d] = A;
-      if (first) {
-        a.ws_m[slot] = mnat;
-        a.ws_l[slot] = L;
+    }
+  } else {
+    // Merge the waves through LDS and store the partition's state.
+    __shared__ float sm[NW][RMAX], sl[NW][RMAX];
+    __shared__ float sacc[NW][RMAX][D];
+    if (tl == 0) {
+#pragma unroll
+      for (int r = 0; r < RMAX; ++r) {
+        if (dc == 0) {
+          sm[wave][r] = m[r];
+          sl[wave][r] = l[r];
+        }
+#pragma unroll
+        for (int i = 0; i < CH; ++i)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) sacc[wave][r][(dc + i * LPR) * 8 + e] = acc[r][i * 8 + e];
+      }
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < a.R * DW; idx += NW * 64) {
+      const int r = idx / DW, d = ds * DW + idx % DW;
+      float M = kNegInf;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) M = fmaxf(M, sm[w][r]);
+      const float ms = (M == kNegInf) ? 0.f : M;
+      float L = 0.f, A = 0.f;
+#pragma unroll
+      for (int w = 0; w < NW; ++w) {
+        const float wt = exp2_fast(sm[w][r] - ms);
+        L = fmaf(wt, sl[w][r], L);
+        A = fmaf(wt, sacc[w][r][d], A);
+      }
+      const size_t slot = (row0 + r) * (size_t)P + p;
+      const float mnat = (M == kNegInf) ? kNegInf : M * kLn2;  // natural-log units
+      // Every channel slice stores the row's reference and sum (the same values):
+      // the combine of a slice waits only for that slice's workgroups.
+      const bool first = idx % DW == 0;
+      if (!FUSED && a.ws_acc == nullptr) {
+        // One partition, no workspace: the state is the row's result.
+        a.o[(row0 + r) * D + d] = (M == kNegInf || L == 0.f) ? 0.f : A / L;
+      } else if constexpr (FUSED) {
+        store_dev(&a.ws_acc[slot * D + d], A);  // read by another workgroup in this launch
+        if (first) {
+          store_dev(&a.ws_m[slot], mnat);
+          store_dev(&a.ws_l[slot], L);
+        }
+      } else {
+        a.ws_acc[slot * D + d] = A;
+        if (first) {
+          a.ws_m[slot] = mnat;
+          a.ws_l[slot] = L;
+        }
       }
     }
   }
