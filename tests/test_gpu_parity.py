@@ -109,6 +109,8 @@ SPLIT_SHAPES = [
     (1, 8, 1, 8, 2000, 128, 0),     # G*Sq = 64: MFMA producer, library-chosen partitions
     (1, 4, 2, 1, 64, 128, 64),      # one partition
     (1, 32, 4, 5, 333, 64, 128),    # G*Sq = 40, D = 64
+    (1, 6, 2, 1, 900, 128, 256),    # G*Sq = 3: padded row block, fused combine
+    (2, 3, 3, 3, 500, 64, 128),     # G*Sq = 3 from three query rows, D = 64
 ]
 
 
