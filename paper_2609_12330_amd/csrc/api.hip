@@ -76,8 +76,8 @@ ef::KeyRuns key_runs(int Sq, int Skv, int window, int sinks) {
 // over the legal schedules, minimise the largest work/throughput ratio over
 // the modelled resources). Resources: HBM (K/V, q, o and the partial states
 // written and read back) and the streaming time of one workgroup (T keys of K
-// and V at that workgroup's rate, times the rounds of workgroups the chip
-// holds); the combine follows (inside the producer for up to 64 partitions,
+// and V, or the fewer keys its rows can see, at that workgroup's rate, times
+// the rounds of workgroups the chip holds); the combine follows (inside the producer for up to 64 partitions,
 // else a second kernel). The rates were fitted to partition-size sweeps of
 // twelve decode shapes on MI355X (1 to 64 query rows per kv head, 1K to 128K
 // keys): the VALU producer streams 6.5 TB/s over the chip and 27.6, 51.1 or
@@ -103,11 +103,13 @@ constexpr double kFusedCombineUsPer16 = 4.4;
 constexpr double kCombineValuUs = 8.9;
 constexpr double kCombineMfmaUs = 13.4;
 
-double split_model_us(const Shape& s, int keys, int T) {
+double split_model_us(const Shape& s, int keys, int T, int visible) {
   const int G = s.Hq / s.Hkv;
   const int R = G * s.Sq;
   const double P = std::ceil((double)keys / T);
   const double Tk = std::min<double>(T, keys);
+  // A workgroup streams at most the keys its rows can see, however long its partition.
+  const double Twg = std::min<double>(Tk, visible);
   const bool valu = R <= kDecodeValuRows;
   double nw, wg_per_part, wg_rate;
   if (valu) {
@@ -135,7 +137,7 @@ double split_model_us(const Shape& s, int keys, int T) {
   const double r_hbm = (kv_bytes + io_bytes + 2.0 * state_bytes) / hbm_eff;
   const double rounds = std::ceil(waves / kResidentWaves);
   const double r_wg =
-      rounds * (Tk * s.D * 4.0 / wg_rate + (valu ? kRoundValuUs : kRoundMfmaUs));
+      rounds * (Twg * s.D * 4.0 / wg_rate + (valu ? kRoundValuUs : kRoundMfmaUs));
   const bool fused = valu && P <= ef::kFusedMaxP;
   const double combine = fused ? kFusedCombineUsPer16 * std::ceil(P / 16.0)
                                : state_bytes / hbm + (valu ? kCombineValuUs : kCombineMfmaUs);
@@ -158,15 +160,34 @@ std::vector<int> partition_candidates(int keys) {
   return out;
 }
 
+// The most keys of the virtual key axis the rows of one workgroup can see: the
+// whole axis without a window; with one, the sink run plus the union of the
+// rows' windows. A workgroup of the matrix-core producer holds the rows of
+// ceil(BM / G) query positions (rows are packed r = sq*G + g), one of the vector
+// producer all Sq of them. A window run cut into partitions leaves each row
+// tile most of its keys in one partition, so splitting it shortens no
+// workgroup's stream (attention-sink prefill: 1024 positions, a 5,123-key run,
+// 4,228 keys per row tile).
+int visible_keys(const Shape& s, const ef::KeyRuns& runs) {
+  if (runs.window <= 0) return runs.lv;
+  const int G = s.Hq / s.Hkv;
+  const int R = G * s.Sq;
+  const int pos = R <= kDecodeValuRows
+                      ? s.Sq
+                      : std::min(s.Sq, (ef::mfma_rows_per_block(R) + G - 1) / G);
+  const long long v = (long long)runs.window + runs.sinks + pos;
+  return (int)std::min<long long>(runs.lv, v);
+}
+
 // Keys per partition of a key axis of `keys` keys (the visible runs' length):
 // the caller's choice, else the candidate the model rates fastest.
-int resolve_partition(const Shape& s, int keys, int partition_size) {
+int resolve_partition(const Shape& s, int keys, int partition_size, int visible) {
   if (partition_size > 0) return partition_size;
   if (keys <= 0) return kTileKeys;
   int best = kTileKeys;
   double best_us = 1e300;
   for (int t : partition_candidates(keys)) {
-    const double us = split_model_us(s, keys, t);
+    const double us = split_model_us(s, keys, t, visible);
     if (us < best_us) {
       best_us = us;
       best = t;
@@ -268,14 +289,14 @@ ef_status fwd_impl(const Shape& s, const void* q, const void* k, const void* v, 
 int partition_size_impl(const Shape& s, const ef::KeyRuns& runs, int partition_size) {
   if (check_shape(s) != EF_OK) return 0;
   if (partition_size < 0 || partition_size % kTileKeys != 0) return 0;
-  return resolve_partition(s, runs.lv, partition_size);
+  return resolve_partition(s, runs.lv, partition_size, visible_keys(s, runs));
 }
 
 size_t workspace_size_impl(const Shape& s, const ef::KeyRuns& runs, int partition_size) {
   if (check_shape(s) != EF_OK) return 0;
   if (partition_size < 0 || partition_size % kTileKeys != 0) return 0;
   if (s.rows() == 0 || s.Skv == 0) return 0;
-  const int T = resolve_partition(s, runs.lv, partition_size);
+  const int T = resolve_partition(s, runs.lv, partition_size, visible_keys(s, runs));
   const long long P = (runs.lv + (long long)T - 1) / T;
   return ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv).bytes;
 }
@@ -347,7 +368,7 @@ ef_status split_prepare(const Shape& s, const void* q, const void* k, const void
   *T_out = 0;
   *P_out = 0;
   if (s.rows() == 0 || s.Skv == 0) return EF_OK;
-  const int T = resolve_partition(s, runs.lv, partition_size);
+  const int T = resolve_partition(s, runs.lv, partition_size, visible_keys(s, runs));
   const long long P = (runs.lv + (long long)T - 1) / T;
   if (P > kMaxGridYZ) return EF_ERR_INVALID_PARTITION;
   const WsLayout w = ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv);
@@ -495,7 +516,7 @@ double ef_attention_splitkv_modeled_us(int B, int Hq, int Hkv, int Sq, int Skv, 
   if (partition_size <= 0 || partition_size % kTileKeys != 0) return -1.0;
   const ef::KeyRuns runs = key_runs(Sq, Skv, window, sinks);
   if (s.rows() == 0 || runs.lv == 0) return 0.0;
-  return split_model_us(s, runs.lv, partition_size);
+  return split_model_us(s, runs.lv, partition_size, visible_keys(s, runs));
 }
 
 ef_status ef_attention_splitkv_tune(const void* q, const void* k, const void* v, float* o, int B,
@@ -512,14 +533,14 @@ ef_status ef_attention_splitkv_tune(const void* q, const void* k, const void* v,
   const bool local = window > 0;
   const ef::KeyRuns runs = key_runs(Sq, Skv, window, sinks);
   if (s.rows() == 0 || runs.lv == 0) {
-    *partition_size = resolve_partition(s, runs.lv, 0);
+    *partition_size = resolve_partition(s, runs.lv, 0, visible_keys(s, runs));
     return EF_OK;
   }
   // Candidates the model rates best, whose workspace fits.
   std::vector<std::pair<double, int>> ranked;
   for (int t : partition_candidates(runs.lv)) {
     if (workspace_size_impl(s, runs, t) <= workspace_bytes)
-      ranked.push_back({split_model_us(s, runs.lv, t), t});
+      ranked.push_back({split_model_us(s, runs.lv, t, visible_keys(s, runs)), t});
   }
   if (ranked.empty()) return EF_ERR_WORKSPACE_TOO_SMALL;
   std::sort(ranked.begin(), ranked.end());
@@ -579,7 +600,7 @@ long long diff_partitions(const Shape& s, int partition_size, int* T_out) {
   if (check_shape(s) != EF_OK) return 0;
   if (partition_size < 0 || partition_size % kTileKeys != 0) return 0;
   if (s.rows() == 0 || s.Skv == 0) return 1;
-  const int T = resolve_partition(s, s.Skv, partition_size);
+  const int T = resolve_partition(s, s.Skv, partition_size, s.Skv);
   *T_out = T;
   return (s.Skv + (long long)T - 1) / T;
 }
@@ -679,7 +700,7 @@ long long dsplit_partitions(const Shape& s, int d_splits, int partition_size, in
   if ((long long)(s.Hq / s.Hkv) * s.Sq > kDecodeMaxRows) return 0;
   if (partition_size < 0 || partition_size % kTileKeys != 0) return 0;
   if (s.rows() == 0 || s.Skv == 0) return 1;
-  const int T = resolve_partition(s, s.Skv, partition_size);
+  const int T = resolve_partition(s, s.Skv, partition_size, s.Skv);
   *T_out = T;
   return (s.Skv + (long long)T - 1) / T;
 }

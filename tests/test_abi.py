@@ -330,6 +330,11 @@ def test_roofline_partition_choice():
     assert ps(2, 32, 8, 1, 2048, 128, 0) == 128
     # sink decode (4 sinks + 4096-key window of 32768): 2048 keys, 89 us vs 121 us at 64
     assert ef.ef_attention_splitkv_local_partition_size(8, 32, 32, 1, 32768, 128, 4096, 4, 0) == 2048
+    # attention-sink prefill (1024 positions, 4 sinks + 4096-key window of 32768): a row tile
+    # sees 4228 keys of the 5123-key run, so one partition; measured 98-108 us, against
+    # 110-114 us in three partitions and 120-136 us in two
+    T = ef.ef_attention_splitkv_local_partition_size(1, 32, 32, 1024, 32768, 128, 4096, 4, 0)
+    assert ef.splitkv_partitions(1024, 32768, T, 4096, 4) == 1
     for shape in [(8, 32, 8, 1, 4096, 128), (1, 32, 8, 1, 131072, 128), (16, 64, 8, 8, 8192, 128),
                   (2, 8, 2, 3, 900, 128), (1, 4, 4, 1, 70, 64)]:
         t = ps(*shape, 0)
