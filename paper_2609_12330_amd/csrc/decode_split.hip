@@ -259,34 +259,58 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& a, const in
 #pragma unroll
   for (int r = 0; r < RMAX; ++r) m[r] = (m[r] == kNegInf) ? kNegInf : m[r] * c;
 
-  // Merge the row groups of the wave: lanes LPR, 2 LPR, ... apart hold the same
-  // value elements of other keys.
-  auto merge_groups = [&](auto off_tag) {
+  // Merge the row groups of the wave (lanes LPR, 2 LPR, ... apart hold the same
+  // value elements of other keys): the row's largest reference over the groups
+  // first, each lane's state scaled to it once, then plain sums. Every group
+  // ends with the same merged state (each exchange combines the pair in the same
+  // order on both sides, or with a commutative operation).
+  float mx[RMAX];
+#pragma unroll
+  for (int r = 0; r < RMAX; ++r) mx[r] = m[r];
+  auto max_over = [&](auto off_tag) {
     constexpr int OFF = decltype(off_tag)::value;
     if constexpr (OFF < 64) {
 #pragma unroll
       for (int r = 0; r < RMAX; ++r) {
-        float ma, mb, la_, lb;
-        lane_pair<OFF>(m[r], ma, mb);
-        lane_pair<OFF>(l[r], la_, lb);
-        const float mn = fmaxf(ma, mb);
-        const float ms = (mn == kNegInf) ? 0.f : mn;
-        const float wa = exp2_fast(ma - ms), wb = exp2_fast(mb - ms);
-        l[r] = la_ * wa + lb * wb;
-#pragma unroll
-        for (int e = 0; e < DL; ++e) {
-          float xa, xb;
-          lane_pair<OFF>(acc[r][e], xa, xb);
-          acc[r][e] = xa * wa + xb * wb;
-        }
-        m[r] = mn;
+        float xa, xb;
+        lane_pair<OFF>(mx[r], xa, xb);
+        mx[r] = fmaxf(xa, xb);
       }
     }
   };
-  merge_groups(std::integral_constant<int, LPR>{});
-  merge_groups(std::integral_constant<int, 2 * LPR>{});
-  merge_groups(std::integral_constant<int, 4 * LPR>{});
-  merge_groups(std::integral_constant<int, 8 * LPR>{});
+  auto sum_over = [&](auto off_tag) {
+    constexpr int OFF = decltype(off_tag)::value;
+    if constexpr (OFF < 64) {
+#pragma unroll
+      for (int r = 0; r < RMAX; ++r) {
+        float xa, xb;
+        lane_pair<OFF>(l[r], xa, xb);
+        l[r] = xa + xb;
+#pragma unroll
+        for (int e = 0; e < DL; ++e) {
+          lane_pair<OFF>(acc[r][e], xa, xb);
+          acc[r][e] = xa + xb;
+        }
+      }
+    }
+  };
+  max_over(std::integral_constant<int, LPR>{});
+  max_over(std::integral_constant<int, 2 * LPR>{});
+  max_over(std::integral_constant<int, 4 * LPR>{});
+  max_over(std::integral_constant<int, 8 * LPR>{});
+#pragma unroll
+  for (int r = 0; r < RMAX; ++r) {
+    const float ms = (mx[r] == kNegInf) ? 0.f : mx[r];
+    const float w = exp2_fast(m[r] - ms);  // 0 for a group that saw no key
+    l[r] *= w;
+#pragma unroll
+    for (int e = 0; e < DL; ++e) acc[r][e] *= w;
+    m[r] = mx[r];
+  }
+  sum_over(std::integral_constant<int, LPR>{});
+  sum_over(std::integral_constant<int, 2 * LPR>{});
+  sum_over(std::integral_constant<int, 4 * LPR>{});
+  sum_over(std::integral_constant<int, 8 * LPR>{});
 
   const int P = a.P;
   if constexpr (NW == 1) {
