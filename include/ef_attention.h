@@ -222,13 +222,13 @@ ef_status ef_attention_combine(const float* m, const float* l, const float* acc,
  * Modelled duration in microseconds of one split-KV call with
  * `partition_size` keys per partition (window = sinks = 0 for the causal or
  * full entry point; a local window otherwise). The model is the roofline rule
- * of section 6.3 (over legal schedules, minimise the largest work/throughput
- * ratio over resources): the larger of the HBM time (K/V, q, o and the partial
- * states written and read) and one workgroup's streaming time times the rounds
- * of workgroups the chip holds, plus the combine, with rates measured on
- * MI355X. With partition_size = 0 the split-KV entry points take the
- * candidate (64, 128, 256, 512, ... keys, and one partition holding every
- * key) this model rates fastest.
+ * of section 6.2, static family ranking (over legal schedules, minimise the
+ * largest work/throughput ratio over resources): the larger of the HBM time
+ * (K/V, q, o and the partial states written and read) and one workgroup's
+ * streaming time times the rounds of workgroups the chip holds, plus the
+ * combine, with rates measured on MI355X. With partition_size = 0 the
+ * split-KV entry points take the candidate (64, 128, 256, 512, ... keys, and
+ * one partition holding every key) this model rates fastest.
  * Returns a negative value for invalid arguments.
  */
 double ef_attention_splitkv_modeled_us(int B, int Hq, int Hkv, int Sq, int Skv, int D,

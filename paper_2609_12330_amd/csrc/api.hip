@@ -72,7 +72,7 @@ ef::KeyRuns key_runs(int Sq, int Skv, int window, int sinks) {
   return r;
 }
 
-// Roofline model of one split-KV call with T keys per partition (section 6.3:
+// Roofline model of one split-KV call with T keys per partition (section 6.2,
 // over the legal schedules, minimise the largest work/throughput ratio over
 // the modelled resources). Resources: HBM (K/V, q, o and the partial states
 // written and read back) and the streaming time of one workgroup (T keys of K

@@ -6,13 +6,18 @@
 //
 // Visibility across workgroups (and across the chip's XCDs, whose L2 caches
 // are not coherent with each other): the producer stores its state with
-// device-scope stores (global_store ... sc1), which are written through to the
-// device coherence point; before taking a ticket each thread waits for those
-// stores to complete; the last workgroup reads the states with device-scope
-// loads (sc1), which do not hit stale lines in its own L2. This orders the
-// states before the ticket without the full L2 write-back/invalidate of a
-// device-scope release/acquire fence, which costs more than the whole
-// producer when every workgroup issues one.
+// device-scope stores (sc1), which are written through to the device
+// coherence point and count in the wave's vector-memory counter until that
+// point acknowledges them. Before the workgroup barrier every wave waits for
+// that counter to drain (s_waitcnt vmcnt(0)), so when the ticket is taken all
+// of the workgroup's state stores are visible at device scope; the last
+// workgroup then reads the states with device-scope loads (sc1), which do not
+// hit stale lines in its own L2. This orders the states before the ticket
+// without the full L2 write-back/invalidate of a device-scope release/acquire
+// fence, which costs more than the whole producer when every workgroup issues
+// one. (A workgroup-scope release fence alone is not enough on this chip: it
+// only orders the stores for the workgroup's own L2 view and compiles to no
+// wait at all.)
 #pragma once
 
 #include "ef_device.hpp"
@@ -33,7 +38,11 @@ __device__ __forceinline__ float load_dev(const float* p) {
 // workgroup that arrives last.
 __device__ __forceinline__ bool last_of_group(unsigned* counter, int arrivals) {
   __shared__ unsigned ticket;
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");  // waits for the stores above
+  // Compiler ordering: no store above may sink below this point.
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+  // Hardware ordering: this wave's device-scope state stores have been
+  // acknowledged (vmcnt(0); expcnt and lgkmcnt left at their maximum).
+  __builtin_amdgcn_s_waitcnt(0x0f70);
   __syncthreads();
   if (threadIdx.x == 0)
     ticket = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -213,6 +213,66 @@ def test_golden_combine_cases():
         np.testing.assert_allclose(o, np.array(val(c["o"])), rtol=0, atol=1e-14)
 
 
+def _golden_error_scale_cases():
+    """The hand-derived (sum_p w_p |acc_p|) / L cases, as float64 arrays."""
+    from fractions import Fraction
+
+    consts = {"ln2": math.log(2.0), "ln3": math.log(3.0), "-inf": -math.inf}
+
+    def val(x):
+        if isinstance(x, list):
+            return [val(y) for y in x]
+        if isinstance(x, str):
+            return consts[x] if x in consts else float(Fraction(x))
+        return float(x)
+
+    return [(c["name"], *(np.array(val(c[key])) for key in ("m", "l", "acc", "scale", "o")))
+            for c in json.load(open(GOLDEN))["combine_error_scale"]]
+
+
+def _error_scale_pins(fn):
+    """Largest deviation of fn(m, l, acc) from the golden error scales."""
+    return max(float(np.max(np.abs(fn(m, l, acc) - scale)))
+               for _, m, l, acc, scale, _ in _golden_error_scale_cases())
+
+
+def test_golden_combine_error_scale_cases():
+    """The magnitude the fp32 combine bar is relative to, on hand-derived P > 1 cases
+    (weights 1/2 and 1/3, cancelling signs, an identity partition, an empty row)."""
+    for name, m, l, acc, scale, o in _golden_error_scale_cases():
+        np.testing.assert_allclose(oracle.combine_error_scale(m, l, acc), scale, rtol=0,
+                                   atol=1e-14, err_msg=name)
+        np.testing.assert_allclose(oracle.combine_ref(m, l, acc), o, rtol=0, atol=1e-14,
+                                   err_msg=name)
+    assert _error_scale_pins(oracle.combine_error_scale) <= 1e-14
+
+
+def _error_scale_mutant(kind):
+    """combine_error_scale with one planted mistake."""
+
+    def fn(m, l, acc):
+        M = m.max(axis=1, initial=-np.inf)
+        live = np.isfinite(M)
+        ref = np.where(live, M, 0.0)
+        w = np.where(np.isfinite(m), np.exp(m - ref[:, None]), 0.0)
+        if kind == "weights_dropped":
+            num = np.abs(acc).sum(axis=1)
+        elif kind == "abs_dropped":
+            num = np.einsum("rp,rpd->rd", w, acc)
+        else:
+            num = np.einsum("rp,rpd->rd", w, np.abs(acc))
+        L = l.sum(axis=1) if kind == "unweighted_sum" else (w * l).sum(axis=1)
+        return np.where(live[:, None], num / np.where(L > 0, L, 1.0)[:, None], 0.0)
+
+    return fn
+
+
+@pytest.mark.parametrize("kind", ["weights_dropped", "abs_dropped", "unweighted_sum"])
+def test_mutant_combine_error_scale(kind):
+    assert _error_scale_pins(_error_scale_mutant(kind)) > 1e-6
+    assert _error_scale_pins(_error_scale_mutant("none")) <= 1e-14
+
+
 # ---------------------------------------------------------------------------
 # Invariants
 # ---------------------------------------------------------------------------
