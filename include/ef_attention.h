@@ -53,7 +53,7 @@
 extern "C" {
 #endif
 
-#define EF_ABI_VERSION 1
+#define EF_ABI_VERSION 2
 
 typedef enum {
   EF_OK = 0,
@@ -116,10 +116,10 @@ int ef_attention_splitkv_partition_size(int B, int Hq, int Hkv, int Sq, int Skv,
  * Bytes of workspace ef_attention_splitkv needs for these sizes (0 when the
  * arguments are invalid or nothing is computed). With rows = B*Hq*Sq,
  * P = ceil(Skv / T) and T the resolved partition size, the workspace holds
- *     m   [rows][P]    fp32 at byte 0
- *     l   [rows][P]    fp32 at byte  A = round_up(rows*P*4, 256)
- *     acc [rows][P][D] fp32 at byte 2*A
- *     counters [B*Hkv][64] uint32 at byte C = round_up(2*A + rows*P*D*4, 256)
+ *     counters [512][64] uint32 at byte 0 (EF_COUNTER_REGION_BYTES)
+ *     m   [rows][P]    fp32 at byte  C = EF_COUNTER_REGION_BYTES
+ *     l   [rows][P]    fp32 at byte  C + A, A = round_up(rows*P*4, 256)
+ *     acc [rows][P][D] fp32 at byte  C + 2*A
  * with row = (b*Hq + hq)*Sq + sq: a reference point m for the scaled scores
  * s of the row's visible keys in partition p (natural-log units; at most the
  * partition maximum and within 8*ln(2) of it), l = sum exp(s - m) and
@@ -127,8 +127,12 @@ int ef_attention_splitkv_partition_size(int B, int Hq, int Hkv, int Sq, int Skv,
  * describe the same state. A partition with no visible key holds the reducer
  * identity (-inf, 0, 0). The counters are arrival counters of the fused
  * combine (see ef_attention_splitkv): word 0 of each 256-byte slot
- * counters[b*Hkv + hk] serves one (batch, kv head); the rest is padding.
+ * counters[b*Hkv + hk] serves one (batch, kv head); the rest is padding. The
+ * counter region has the same place and size for every problem, and no
+ * partial state is ever stored in it.
  */
+#define EF_COUNTER_REGION_BYTES ((size_t)512 * 256)
+
 size_t ef_attention_splitkv_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
                                            int partition_size);
 
@@ -147,16 +151,22 @@ size_t ef_attention_splitkv_workspace_size(int B, int Hq, int Hkv, int Sq, int S
  *                      ef_attention_splitkv_workspace_size(...) bytes,
  *                      16-byte aligned; on return (stream-ordered) it holds
  *                      the partial states in the layout documented there.
- *                      Its counter region must be zero before the first call
- *                      that uses it (zero-fill the new buffer once); every
- *                      call leaves it zero again, so a workspace serves any
- *                      number of calls in stream order. Calls that overlap
- *                      in time must not share a workspace.
+ *                      Its counter region (the first EF_COUNTER_REGION_BYTES)
+ *                      must be zero before the first call that uses it
+ *                      (zero-fill the new buffer once); every completed call
+ *                      leaves it zero again, so a workspace serves any number
+ *                      of calls of any shapes whose workspace fits in it, in
+ *                      stream order. Calls that overlap in time must not share
+ *                      a workspace.
  *   workspace_bytes  : its size in bytes.
- * When G*Sq <= 4 and P <= 64 the combine runs inside the producer: the last
- * workgroup of each (batch, kv head) to store its state, found with the
- * group's arrival counter, combines that group's rows and resets the counter
- * (one kernel instead of two). Otherwise a separate combine kernel follows.
+ * When G*Sq <= 4, P <= 64 and B*Hkv <= 512 the combine runs inside the
+ * producer: the last workgroup of each (batch, kv head) to store its state,
+ * found with the group's arrival counter, combines that group's rows and
+ * resets the counter (one kernel instead of two). Otherwise a separate combine
+ * kernel follows. A counter that is not zero when the call begins (a counter
+ * region never cleared) cannot tell which workgroup is last; the producer
+ * then fills that group's output rows with NaN rather than combine states
+ * that may be stale.
  * Other arguments as for ef_attention_fwd.
  */
 ef_status ef_attention_splitkv(const void* q, const void* k, const void* v, float* o,
@@ -315,8 +325,9 @@ size_t ef_diff_attention_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv,
  *            channels of o directly: no workspace (it may be NULL) and no
  *            merge. Otherwise the workspace (ef_attention_decode_dsplit_workspace_size
  *            bytes, 16-byte aligned, counters zero on entry and left zero, as for
- *            ef_attention_splitkv) holds the states, which every channel slice
- *            combines for its own channels.
+ *            ef_attention_splitkv; counter slot (b*Hkv + hk)*d_splits + slice)
+ *            holds the states, which every channel slice combines for its own
+ *            channels (in the producer when P <= 64 and B*Hkv*d_splits <= 512).
  */
 ef_status ef_attention_decode_dsplit(const void* q, const void* k, const void* v, float* o,
                                      int B, int Hq, int Hkv, int Sq, int Skv, int D,
@@ -325,7 +336,7 @@ ef_status ef_attention_decode_dsplit(const void* q, const void* k, const void* v
 
 /*
  * Workspace bytes of ef_attention_decode_dsplit: 0 with one partition, else
- * the split-KV layout with B*Hkv*d_splits counter slots. 0 for invalid
+ * the split-KV layout (the same counter region and states). 0 for invalid
  * arguments too.
  */
 size_t ef_attention_decode_dsplit_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,

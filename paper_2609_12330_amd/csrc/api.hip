@@ -17,6 +17,8 @@ constexpr int kDecodeMaxRows = 8;    // the VALU split producer handles G*Sq <= 
 constexpr int kDecodeValuRows = 4;   // ... and the split-KV paths give it G*Sq <= 4 (the MFMA
                                      // producer streams faster with more rows)
 constexpr int kMaxGridYZ = 65535;
+static_assert(ef::kCounterRegionBytes == EF_COUNTER_REGION_BYTES,
+              "the counter region of the header is the kernels' one");
 
 struct Shape {
   int B, Hq, Hkv, Sq, Skv, D;
@@ -138,7 +140,7 @@ double split_model_us(const Shape& s, int keys, int T, int visible) {
   const double rounds = std::ceil(waves / kResidentWaves);
   const double r_wg =
       rounds * (Twg * s.D * 4.0 / wg_rate + (valu ? kRoundValuUs : kRoundMfmaUs));
-  const bool fused = valu && P <= ef::kFusedMaxP;
+  const bool fused = valu && P <= ef::kFusedMaxP && kv_heads <= ef::kCounterSlots;
   const double combine = fused ? kFusedCombineUsPer16 * std::ceil(P / 16.0)
                                : state_bytes / hbm + (valu ? kCombineValuUs : kCombineMfmaUs);
   return std::max(r_hbm, r_wg) + combine;
@@ -204,15 +206,25 @@ struct WsLayout {
   size_t m_off, l_off, acc_off, cnt_off, bytes;
 };
 
-WsLayout ws_layout(long long rows, long long P, int D, long long kv_heads) {
+// Counters first (a region of fixed size, see kCounterRegionBytes), then the
+// partial states.
+WsLayout ws_layout(long long rows, long long P, int D) {
   WsLayout w;
   const size_t a = ef::ws_align256((size_t)(rows * P) * sizeof(float));
-  w.m_off = 0;
-  w.l_off = a;
-  w.acc_off = 2 * a;
-  w.cnt_off = ef::ws_align256(2 * a + (size_t)(rows * P) * (size_t)D * sizeof(float));
-  w.bytes = w.cnt_off + (size_t)kv_heads * ef::kCounterStride * sizeof(unsigned);
+  w.cnt_off = 0;
+  w.m_off = ef::kCounterRegionBytes;
+  w.l_off = w.m_off + a;
+  w.acc_off = w.m_off + 2 * a;
+  w.bytes = w.acc_off + ef::ws_align256((size_t)(rows * P) * (size_t)D * sizeof(float));
   return w;
+}
+
+// Whether the producer combines the states itself: few query rows per kv head
+// (the vector producer), few partitions, and a counter slot for every group.
+bool fused_combine(const Shape& s, long long P, int d_splits) {
+  return ((long long)(s.Hq / s.Hkv) * s.Sq <= kDecodeValuRows || d_splits > 0) &&
+         P <= ef::kFusedMaxP &&
+         (long long)s.B * s.Hkv * std::max(d_splits, 1) <= ef::kCounterSlots;
 }
 
 ef_status from_hip(hipError_t e) { return e == hipSuccess ? EF_OK : EF_ERR_HIP; }
@@ -298,7 +310,7 @@ size_t workspace_size_impl(const Shape& s, const ef::KeyRuns& runs, int partitio
   if (s.rows() == 0 || s.Skv == 0) return 0;
   const int T = resolve_partition(s, runs.lv, partition_size, visible_keys(s, runs));
   const long long P = (runs.lv + (long long)T - 1) / T;
-  return ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv).bytes;
+  return ws_layout(s.rows(), P, s.D).bytes;
 }
 
 }  // namespace
@@ -371,7 +383,7 @@ ef_status split_prepare(const Shape& s, const void* q, const void* k, const void
   const int T = resolve_partition(s, runs.lv, partition_size, visible_keys(s, runs));
   const long long P = (runs.lv + (long long)T - 1) / T;
   if (P > kMaxGridYZ) return EF_ERR_INVALID_PARTITION;
-  const WsLayout w = ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv);
+  const WsLayout w = ws_layout(s.rows(), P, s.D);
   if (workspace == nullptr || workspace_bytes < w.bytes) return EF_ERR_WORKSPACE_TOO_SMALL;
   if (misaligned(workspace)) return EF_ERR_MISALIGNED;
   char* ws = static_cast<char*>(workspace);
@@ -429,8 +441,7 @@ ef_status splitkv_impl(const Shape& s, const void* q, const void* k, const void*
   if (st != EF_OK || s.rows() == 0) return st;
   hipStream_t hs = static_cast<hipStream_t>(stream);
   if (s.Skv == 0) return from_hip(ef::launch_zero_fill(o, (size_t)s.rows() * s.D, hs));
-  const bool fused = (s.Hq / s.Hkv) * s.Sq <= kDecodeValuRows && P <= ef::kFusedMaxP;
-  if (fused)
+  if (fused_combine(s, P, 0))
     return split_produce(s, q, k, v, scale, causal, runs, T, P, ws_m, ws_l, ws_acc, counters, o,
                          hs);
   st = split_produce(s, q, k, v, scale, causal, runs, T, P, ws_m, ws_l, ws_acc, nullptr, nullptr,
@@ -670,7 +681,7 @@ ef_status ef_diff_attention(const void* q1, const void* q2, const void* k1, cons
     return launch_mfma(s, q1, k1, v, o, nullptr, nullptr, nullptr, runs.lv, 1, scale, causal,
                        runs, hs, &diff);
   }
-  const WsLayout w = ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv);
+  const WsLayout w = ws_layout(s.rows(), P, s.D);
   if (workspace == nullptr || workspace_bytes < w.bytes) return EF_ERR_WORKSPACE_TOO_SMALL;
   if (misaligned(workspace)) return EF_ERR_MISALIGNED;
   char* ws = static_cast<char*>(workspace);
@@ -685,7 +696,7 @@ size_t ef_diff_attention_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv,
   int T = 0;
   const long long P = diff_partitions(s, partition_size, &T);
   if (P <= 1) return 0;
-  return ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv).bytes;
+  return ws_layout(s.rows(), P, s.D).bytes;
 }
 
 }  // extern "C"
@@ -731,7 +742,7 @@ ef_status ef_attention_decode_dsplit(const void* q, const void* k, const void* v
   if (P == 1)  // each workgroup writes its channels of o: no workspace, no merge
     return split_produce(s, q, k, v, scale, causal, runs, T, 1, nullptr, nullptr, nullptr,
                          nullptr, o, hs, d_splits);
-  const WsLayout w = ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv * d_splits);
+  const WsLayout w = ws_layout(s.rows(), P, s.D);
   if (workspace == nullptr || workspace_bytes < w.bytes) return EF_ERR_WORKSPACE_TOO_SMALL;
   if (misaligned(workspace)) return EF_ERR_MISALIGNED;
   char* ws = static_cast<char*>(workspace);
@@ -739,7 +750,7 @@ ef_status ef_attention_decode_dsplit(const void* q, const void* k, const void* v
   float* ws_l = reinterpret_cast<float*>(ws + w.l_off);
   float* ws_acc = reinterpret_cast<float*>(ws + w.acc_off);
   unsigned* counters = reinterpret_cast<unsigned*>(ws + w.cnt_off);
-  if (P <= ef::kFusedMaxP)
+  if (fused_combine(s, P, d_splits))
     return split_produce(s, q, k, v, scale, causal, runs, T, (int)P, ws_m, ws_l, ws_acc,
                          counters, o, hs, d_splits);
   st = split_produce(s, q, k, v, scale, causal, runs, T, (int)P, ws_m, ws_l, ws_acc, nullptr,
@@ -762,7 +773,7 @@ size_t ef_attention_decode_dsplit_workspace_size(int B, int Hq, int Hkv, int Sq,
   int T = 0;
   const long long P = dsplit_partitions(s, d_splits, partition_size, &T);
   if (P <= 1) return 0;
-  return ws_layout(s.rows(), P, s.D, (long long)s.B * s.Hkv * d_splits).bytes;
+  return ws_layout(s.rows(), P, s.D).bytes;
 }
 
 }  // extern "C"

@@ -436,7 +436,12 @@ __device__ __forceinline__ void decode_partition(const DecodeParams& a, const in
     __shared__ float cl[RMAX * kFusedMaxP];
     __shared__ float cinv[RMAX];
     unsigned* counter = a.counters + (((size_t)b * a.Hkv + hkv) * DS + ds) * kCounterStride;
-    if (!last_of_group(counter, P)) return;
+    const unsigned ticket = arrival_ticket(counter);
+    if (ticket >= (unsigned)P) {
+      poison_group<D, DW, NW * 64>(a.o, row0, a.R, ds * DW);
+      return;
+    }
+    if (ticket != (unsigned)(P - 1)) return;
     combine_group<D, DW, NW * 64, RMAX>(a.ws_m, a.ws_l, a.ws_acc, a.o, row0, a.R, P, cw, cl,
                                         cinv, ds * DW);
     if (threadIdx.x == 0) reset_counter(counter);

@@ -56,9 +56,16 @@ struct DecodeParams {
 // Largest partition count for which the producer combines its group itself.
 constexpr int kFusedMaxP = 64;
 
-// Arrival counters sit 256 bytes apart (one counter per (batch, kv head)):
-// counters sharing a line serialise the workgroups' arrivals at the end.
+// Arrival counters sit 256 bytes apart (one counter per (batch, kv head),
+// and channel slice): counters sharing a line serialise the workgroups'
+// arrivals at the end. They occupy a region of fixed size at the start of
+// every workspace, so a workspace reused for problems of other shapes keeps
+// its counters in place (each completed call leaves the slots it used at
+// zero, and no partial state is ever stored there). A launch with more
+// groups than slots combines in a separate kernel instead.
 constexpr int kCounterStride = 64;
+constexpr int kCounterSlots = 512;
+constexpr size_t kCounterRegionBytes = (size_t)kCounterSlots * kCounterStride * 4;
 
 // MFMA attention (single pass, or split producer when ws_m != nullptr).
 struct MfmaParams {

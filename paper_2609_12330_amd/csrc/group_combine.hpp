@@ -34,9 +34,11 @@ __device__ __forceinline__ float load_dev(const float* p) {
 }
 
 // Takes a ticket on the group's arrival counter once this workgroup's
-// device-scope state stores have completed; true in every thread of the
-// workgroup that arrives last.
-__device__ __forceinline__ bool last_of_group(unsigned* counter, int arrivals) {
+// device-scope state stores have completed; returns the ticket (the same in
+// every thread of the workgroup). Tickets run 0 .. arrivals - 1 from a
+// counter that is zero when the launch begins; the workgroup holding
+// arrivals - 1 arrives last.
+__device__ __forceinline__ unsigned arrival_ticket(unsigned* counter) {
   __shared__ unsigned ticket;
   // Compiler ordering: no store above may sink below this point.
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
@@ -47,7 +49,18 @@ __device__ __forceinline__ bool last_of_group(unsigned* counter, int arrivals) {
   if (threadIdx.x == 0)
     ticket = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   __syncthreads();
-  return ticket == (unsigned)(arrivals - 1);
+  return ticket;
+}
+
+// Output rows row0 .. row0 + nrows - 1, channels [d0, d0 + DW), set to NaN. A
+// ticket at or past the arrival count means the counter was not zero when the
+// launch began (a workspace whose counter region was never cleared), so the
+// group's combine cannot be trusted: its rows are made visibly invalid rather
+// than silently stale.
+template <int D, int DW, int NT>
+__device__ __forceinline__ void poison_group(float* o, size_t row0, int nrows, int d0) {
+  for (int i = threadIdx.x; i < nrows * DW; i += NT)
+    o[(row0 + i / DW) * D + d0 + i % DW] = __builtin_nanf("");
 }
 
 __device__ __forceinline__ void reset_counter(unsigned* counter) {

@@ -319,7 +319,8 @@ def splitkv_partitions(Sq, Skv, T, window=0, sinks=0) -> int:
 
 def make_workspace(q, k, partition_size=0, window=0, sinks=0):
     """A zero-filled uint8 tensor on q's GPU large enough for attention_splitkv on these
-    shapes (its arrival counters must start at zero; the library leaves them zero)."""
+    shapes (its arrival counters must start at zero; the library leaves them zero, so the
+    workspace serves later calls of any shape whose workspace fits in it)."""
     torch = _torch()
     if not q.is_cuda:
         raise TypeError("make_workspace needs GPU tensors (the workspace lives on q's device)")
@@ -329,27 +330,29 @@ def make_workspace(q, k, partition_size=0, window=0, sinks=0):
     return torch.zeros(max(n, 256), dtype=torch.uint8, device=q.device)
 
 
+# Arrival-counter region at the start of every split-KV workspace (512 slots of 256 bytes);
+# the partial states follow it.
+COUNTER_REGION_BYTES = 512 * 256
+
+
 def workspace_views(ws, B, Hq, Sq, Skv, D, T, window=0, sinks=0):
     """(m [rows,P], l [rows,P], acc [rows,P,D]) fp32 views of a split-KV workspace."""
     rows = B * Hq * Sq
     P = splitkv_partitions(Sq, Skv, T, window, sinks)
     a = (rows * P * 4 + 255) // 256 * 256
     f = ws.view(_torch().float32) if ws.dtype != _torch().float32 else ws
-    m = f[: rows * P].view(rows, P)
-    l = f[a // 4: a // 4 + rows * P].view(rows, P)
-    acc = f[2 * a // 4: 2 * a // 4 + rows * P * D].view(rows, P, D)
+    base = COUNTER_REGION_BYTES // 4
+    m = f[base: base + rows * P].view(rows, P)
+    l = f[base + a // 4: base + a // 4 + rows * P].view(rows, P)
+    acc = f[base + 2 * a // 4: base + 2 * a // 4 + rows * P * D].view(rows, P, D)
     return m, l, acc
 
 
-def workspace_counters(ws, B, Hq, Hkv, Sq, Skv, D, T, window=0, sinks=0):
-    """int32 view [B*Hkv, 64] of the arrival-counter slots of a split-KV workspace (word 0
-    of each slot is the counter of one (batch, kv head))."""
+def workspace_counters(ws, slots=512):
+    """int32 view [slots, 64] of the arrival-counter region of a split-KV workspace (word 0
+    of each 256-byte slot is the counter of one (batch, kv head, channel slice))."""
     torch = _torch()
-    rows = B * Hq * Sq
-    P = splitkv_partitions(Sq, Skv, T, window, sinks)
-    a = (rows * P * 4 + 255) // 256 * 256
-    c = (2 * a + rows * P * D * 4 + 255) // 256 * 256
-    return ws[c: c + 256 * B * Hkv].view(torch.int32).view(B * Hkv, 64)
+    return ws[: 256 * slots].view(torch.int32).view(slots, 64)
 
 
 def attention_splitkv(q, k, v, scale: Optional[float] = None, causal: bool = False,

@@ -48,7 +48,7 @@ def test_library_exports_every_header_symbol():
     lib = ctypes.CDLL(ef.LIB_PATH)
     for name in header_functions():
         assert hasattr(lib, name), name
-    assert ef.library().ef_abi_version() == 1
+    assert ef.library().ef_abi_version() == 2
 
 
 @needs_lib
@@ -216,9 +216,9 @@ def test_dsplit_specific_validation():
     assert dsplit(ws=None) == 7
     sz = ef.ef_attention_decode_dsplit_workspace_size
     need = sz(1, 4, 2, 1, 1000, 128, 2, 256)
-    # The split-KV layout with B*Hkv*d_splits counter slots.
-    assert need == ef.ef_attention_splitkv_workspace_size(1, 4, 2, 1, 1000, 128, 256) + 2 * 256
-    assert sz(1, 4, 2, 1, 1000, 128, 4, 256) == need + 4 * 256
+    # The split-KV layout: the same fixed counter region and states for every d_splits.
+    assert need == ef.ef_attention_splitkv_workspace_size(1, 4, 2, 1, 1000, 128, 256)
+    assert sz(1, 4, 2, 1, 1000, 128, 4, 256) == need
     assert dsplit(wsb=need - 1) == 7
     assert dsplit(ws=MIS, wsb=need) == 5
     # One partition: no workspace.
@@ -245,9 +245,7 @@ def test_workspace_and_partition_arithmetic():
     ws = ef.ef_attention_splitkv_workspace_size
     ps = ef.ef_attention_splitkv_partition_size
     def layout(rows, P, D, kv_heads):
-        a = (rows * P * 4 + 255) // 256 * 256
-        c = (2 * a + rows * P * D * 4 + 255) // 256 * 256
-        return c + kv_heads * 256
+        return _layout(rows, P, D, kv_heads)
 
     # GQA decode, 256-key partitions: rows = 8*32, P = 16, 64 kv heads
     assert ws(8, 32, 8, 1, 4096, 128, 256) == layout(256, 16, 128, 64)
@@ -269,9 +267,11 @@ def test_workspace_and_partition_arithmetic():
 
 
 def _layout(rows, P, D, kv_heads):
+    """Workspace bytes as the header documents them: the 128 KiB counter region (512 slots
+    of 256 bytes, whatever the number of kv heads), then m, l and acc."""
+    assert kv_heads <= 512
     a = (rows * P * 4 + 255) // 256 * 256
-    c = (2 * a + rows * P * D * 4 + 255) // 256 * 256
-    return c + kv_heads * 256
+    return 512 * 256 + 2 * a + (rows * P * D * 4 + 255) // 256 * 256
 
 
 def _runs(Sq, Skv, W, S):

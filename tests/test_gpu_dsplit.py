@@ -113,14 +113,13 @@ def test_dsplit_workspace_counters_left_zero():
     qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
     n = ef.ef_attention_decode_dsplit_workspace_size(1, 8, 2, 1, 2000, 128, 4, 256)
     ws = torch.full((n,), 0xFF, dtype=torch.uint8, device="cuda")
-    ws[n - 8 * 256:] = 0  # B*Hkv*d_splits = 8 counter slots, zero on entry
+    ws[:ef.COUNTER_REGION_BYTES] = 0  # the counter region, zero on entry
     ref = ef.attention_splitkv(qd, kd, vd, partition_size=256)
     first = ef.attention_decode_dsplit(qd, kd, vd, d_splits=4, partition_size=256, workspace=ws)
     second = ef.attention_decode_dsplit(qd, kd, vd, d_splits=4, partition_size=256, workspace=ws)
     torch.cuda.synchronize()
     assert torch.equal(first, ref) and torch.equal(second, ref)
-    cnt = ws[n - 8 * 256:].view(torch.int32).view(8, 64)
-    assert int(cnt.abs().sum().item()) == 0
+    assert int(ef.workspace_counters(ws).abs().sum().item()) == 0
 
 
 def test_dsplit_mha_decode_workload():

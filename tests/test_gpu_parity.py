@@ -457,7 +457,7 @@ def test_fused_combine_reuses_workspace(shape):
             ws = ef.make_workspace(qd, kd, T)
         o = ef.attention_splitkv(qd, kd, vd, causal=rep == 1, partition_size=T, workspace=ws)
         torch.cuda.synchronize()
-        assert (ef.workspace_counters(ws, B, Hq, Hkv, Sq, Skv, D, T) == 0).all()
+        assert (ef.workspace_counters(ws) == 0).all()
         ref = oracle.attention_ref(f64(q), f64(k), f64(v), 1 / math.sqrt(D), rep == 1)
         assert_close(o, ref, f"fused rep {rep}")
         ws2 = ef.attention_splitkv_partials(qd, kd, vd, causal=rep == 1, partition_size=T)
@@ -465,3 +465,49 @@ def test_fused_combine_reuses_workspace(shape):
         o2 = ef.combine(m.contiguous(), l.contiguous(), acc.contiguous())
         torch.cuda.synchronize()
         assert float((o.reshape(-1, D) - o2).abs().max()) <= 1e-5
+
+
+def test_workspace_reused_across_shapes():
+    """One workspace serves calls of different shapes in turn: the arrival counters sit in a
+    region of fixed place and size at its start, which no call's partial states overwrite
+    (they used to follow the states, so another shape's states landed on them)."""
+    announce("workspace reuse across shapes")
+    shapes = [(8, 32, 8, 1, 4096, 128, 256, False), (2, 8, 2, 1, 1000, 128, 256, True),
+              (1, 6, 2, 1, 900, 128, 64, False), (8, 32, 8, 1, 4096, 128, 256, True)]
+    need = max(ef.splitkv_workspace_size(B, Hq, Hkv, Sq, Skv, D, T)
+               for B, Hq, Hkv, Sq, Skv, D, T, _ in shapes)
+    ws = torch.zeros(need, dtype=torch.uint8, device="cuda")
+    for i, (B, Hq, Hkv, Sq, Skv, D, T, causal) in enumerate(shapes):
+        q, k, v = inputs(B, Hq, Hkv, Sq, Skv, D, seed=700 + i)
+        o = ef.attention_splitkv(q.cuda(), k.cuda(), v.cuda(), causal=causal, partition_size=T,
+                                 workspace=ws)
+        torch.cuda.synchronize()
+        assert int(ef.workspace_counters(ws).abs().sum()) == 0
+        ref = oracle.attention_ref(f64(q), f64(k), f64(v), 1 / math.sqrt(D), causal)
+        assert_close(o, ref, f"reuse call {i}")
+
+
+def test_uncleared_counter_poisons_its_group():
+    """A counter that is not zero when the call begins (a workspace whose counter region was
+    never cleared) makes that group's output NaN instead of silently stale; the other groups
+    are unaffected, and after the region is cleared the workspace works again."""
+    announce("uncleared counter")
+    B, Hq, Hkv, Sq, Skv, D, T = 2, 8, 2, 1, 1000, 128, 256
+    q, k, v = inputs(B, Hq, Hkv, Sq, Skv, D, seed=710)
+    qd, kd, vd = q.cuda(), k.cuda(), v.cuda()
+    ws = ef.make_workspace(qd, kd, T)
+    ws[:ef.COUNTER_REGION_BYTES].view(torch.int32).view(512, 64)[3, 0] = 1000  # (b 1, hkv 1)
+    o = ef.attention_splitkv(qd, kd, vd, partition_size=T, workspace=ws)
+    torch.cuda.synchronize()
+    G = Hq // Hkv
+    bad = o[1, G:2 * G]
+    assert torch.isnan(bad).all()
+    mask = torch.ones(B, Hq, dtype=torch.bool)
+    mask[1, G:2 * G] = False
+    ref = oracle.attention_ref(f64(q), f64(k), f64(v), 1 / math.sqrt(D), False)
+    good = o.cpu().double().numpy()[mask.numpy()]
+    assert_close(good, ref[mask.numpy()], "groups with cleared counters")
+    ws[:ef.COUNTER_REGION_BYTES] = 0
+    o = ef.attention_splitkv(qd, kd, vd, partition_size=T, workspace=ws)
+    torch.cuda.synchronize()
+    assert_close(o, ref, "after clearing")
