@@ -68,7 +68,8 @@ typedef enum {
   EF_ERR_HIP = 9,                  /* HIP reported an error when the work was enqueued */
   EF_ERR_INVALID_MASK = 10,        /* local attention: window < 1 or sinks < 0 */
   EF_ERR_INVALID_DIFF = 11,        /* differential attention: lambda_init or eps not finite, or eps < 0 */
-  EF_ERR_INVALID_SPLIT = 12        /* d_splits not 1, 2 or 4, or more than 8 query rows per kv head */
+  EF_ERR_INVALID_SPLIT = 12,       /* d_splits not 1, 2 or 4, or more than 8 query rows per kv head */
+  EF_ERR_SCRATCH_TOO_SMALL = 13    /* the problem needs more than EF_STATIC_SCRATCH_BYTES of scratch */
 } ef_status;
 
 /* Version of this ABI (EF_ABI_VERSION). */
@@ -341,6 +342,35 @@ ef_status ef_attention_decode_dsplit(const void* q, const void* k, const void* v
  */
 size_t ef_attention_decode_dsplit_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv, int D,
                                                  int d_splits, int partition_size);
+
+/*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * ef_attention_splitkv with the workspace replaced by a scratch array of
+ * static device storage that the library holds, EF_STATIC_SCRATCH_BYTES per
+ * device. The array is reserved when the library's code object is loaded on
+ * a device and held until the process ends; the call itself allocates
+ * nothing. The first call on a device also looks up that device's copy of
+ * the array (a host-side query, not a stream operation), so make it outside
+ * graph capture.
+ *   Arguments, validation and output: as ef_attention_splitkv, without
+ *   `workspace` and `workspace_bytes`. Returns EF_ERR_SCRATCH_TOO_SMALL, with
+ *   nothing enqueued, when ef_attention_splitkv_workspace_size(...) for these
+ *   arguments exceeds EF_STATIC_SCRATCH_BYTES (every other argument error is
+ *   reported first), and EF_ERR_HIP when the scratch array cannot be found on
+ *   the current device.
+ * Every call on one device shares that device's scratch, which keeps the last
+ * call's partial states: calls that overlap in time on one device race with
+ * each other and must be ordered (e.g. issued on one stream). The arrival
+ * counters in the scratch start at zero and every completed call leaves them
+ * at zero.
+ */
+#define EF_STATIC_SCRATCH_BYTES ((size_t)32 << 20)
+
+ef_status ef_attention_splitkv_noalloc(const void* q, const void* k, const void* v, float* o,
+                                       int B, int Hq, int Hkv, int Sq, int Skv, int D,
+                                       float scale, int causal, int partition_size,
+                                       void* stream);
 
 #ifdef __cplusplus
 }

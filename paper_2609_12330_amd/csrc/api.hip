@@ -277,6 +277,8 @@ const char* ef_status_string(int status) {
     case EF_ERR_INVALID_DIFF: return "lambda_init and eps must be finite and eps >= 0";
     case EF_ERR_INVALID_SPLIT:
       return "d_splits must be 1, 2 or 4, with at most 8 query rows per kv head";
+    case EF_ERR_SCRATCH_TOO_SMALL:
+      return "the problem needs more workspace than the library's static scratch holds";
     default: return "unknown status";
   }
 }
@@ -459,6 +461,21 @@ ef_status splitkv_impl(const Shape& s, const void* q, const void* k, const void*
 }
 
 }  // namespace
+
+namespace ef {
+
+// ef_attention_splitkv over a caller-chosen workspace, for the library's other
+// entry points (the allocation-free variant passes its static scratch).
+ef_status splitkv_into(const void* q, const void* k, const void* v, float* o, int B, int Hq,
+                       int Hkv, int Sq, int Skv, int D, float scale, int causal,
+                       int partition_size, void* workspace, size_t workspace_bytes,
+                       void* stream) {
+  return splitkv_impl(Shape{B, Hq, Hkv, Sq, Skv, D}, q, k, v, o, scale, causal,
+                      key_runs(Sq, Skv, 0, 0), partition_size, workspace, workspace_bytes,
+                      stream);
+}
+
+}  // namespace ef
 
 extern "C" {
 

@@ -32,7 +32,11 @@ STATUS_NAMES = {
     10: "EF_ERR_INVALID_MASK",
     11: "EF_ERR_INVALID_DIFF",
     12: "EF_ERR_INVALID_SPLIT",
+    13: "EF_ERR_SCRATCH_TOO_SMALL",
 }
+
+# Bytes of static scratch behind ef_attention_splitkv_noalloc (EF_STATIC_SCRATCH_BYTES).
+STATIC_SCRATCH_BYTES = 32 << 20
 
 # Exported symbols and their C signatures (restype, argtypes).
 _vp, _fp, _i, _f, _sz = ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
@@ -61,6 +65,8 @@ SIGNATURES = {
     "ef_attention_decode_dsplit": (_i, [_vp, _vp, _vp, _fp, _i, _i, _i, _i, _i, _i, _f, _i, _i,
                                         _i, _vp, _sz, _vp]),
     "ef_attention_decode_dsplit_workspace_size": (_sz, [_i, _i, _i, _i, _i, _i, _i, _i]),
+    "ef_attention_splitkv_noalloc": (_i, [_vp, _vp, _vp, _fp, _i, _i, _i, _i, _i, _i, _f, _i,
+                                          _i, _vp]),
 }
 
 
@@ -120,6 +126,12 @@ def ef_attention_splitkv_partials(q, k, v, B, Hq, Hkv, Sq, Skv, D, scale, causal
     return _lib().ef_attention_splitkv_partials(q, k, v, B, Hq, Hkv, Sq, Skv, D, scale,
                                                 int(causal), partition_size, workspace,
                                                 workspace_bytes, stream)
+
+
+def ef_attention_splitkv_noalloc(q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale, causal,
+                                 partition_size, stream) -> int:
+    return _lib().ef_attention_splitkv_noalloc(q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale,
+                                               int(causal), partition_size, stream)
 
 
 def ef_diff_attention(q1, q2, k1, k2, v, o, lambda_q1, lambda_k1, lambda_q2, lambda_k2,
@@ -381,6 +393,21 @@ def attention_splitkv(q, k, v, scale: Optional[float] = None, causal: bool = Fal
                               workspace.data_ptr(), workspace.numel() * workspace.element_size(),
                               _stream_handle(stream))
     _check(st, "ef_attention_splitkv")
+    return o
+
+
+def attention_splitkv_noalloc(q, k, v, scale: Optional[float] = None, causal: bool = False,
+                              partition_size: int = 0, out=None, stream=None):
+    """Split-KV attention through ef_attention_splitkv_noalloc: the library's static
+    scratch holds the partial states, so no workspace is passed; returns o (fp32)."""
+    B, Hq, Hkv, Sq, Skv, D = _check_qkv(q, k, v)
+    if scale is None:
+        scale = 1.0 / math.sqrt(D)
+    o = _out(q, out)
+    st = ef_attention_splitkv_noalloc(q.data_ptr(), k.data_ptr(), v.data_ptr(), o.data_ptr(), B,
+                                      Hq, Hkv, Sq, Skv, D, float(scale), causal, partition_size,
+                                      _stream_handle(stream))
+    _check(st, "ef_attention_splitkv_noalloc")
     return o
 
 

@@ -117,9 +117,19 @@ def dsplit(**kw):
                                          a["stream"])
 
 
+def noalloc(**kw):
+    a = dict(q=A, k=A, v=A, o=A, B=1, Hq=4, Hkv=2, Sq=1, Skv=1000, D=128, scale=0.1, causal=0,
+             T=256, stream=None)
+    a.update(kw)
+    return ef.ef_attention_splitkv_noalloc(a["q"], a["k"], a["v"], a["o"], a["B"], a["Hq"],
+                                           a["Hkv"], a["Sq"], a["Skv"], a["D"], a["scale"],
+                                           a["causal"], a["T"], a["stream"])
+
+
 @needs_lib
-@pytest.mark.parametrize("call", [fwd, split, fwd_local, split_local, diff, dsplit],
-                         ids=["fwd", "splitkv", "fwd_local", "splitkv_local", "diff", "dsplit"])
+@pytest.mark.parametrize("call", [fwd, split, fwd_local, split_local, diff, dsplit, noalloc],
+                         ids=["fwd", "splitkv", "fwd_local", "splitkv_local", "diff", "dsplit",
+                              "noalloc"])
 def test_validation_errors(call):
     assert call(D=96) == 4
     assert call(D=0) == 4
@@ -165,6 +175,21 @@ def test_splitkv_local_specific_validation():
     assert split_local(ws=None) == 7
     assert split_local(T=100) == 6
     assert split_local(ws=MIS, wsb=need) == 5
+
+
+@needs_lib
+def test_noalloc_specific_validation():
+    """The static-scratch entry point: partition errors as for the workspace path, and a
+    problem whose workspace exceeds the scratch is refused (after every other check)."""
+    assert noalloc(T=100) == 6
+    big = dict(B=16, Hq=64, Hkv=8, Sq=8, Skv=8192, T=256)
+    assert ef.ef_attention_splitkv_workspace_size(16, 64, 8, 8, 8192, 128, 256) > \
+        ef.STATIC_SCRATCH_BYTES
+    assert noalloc(**big) == 13
+    assert noalloc(q=None, **big) == 1
+    assert noalloc(o=MIS, **big) == 5
+    assert noalloc(scale=math.nan, **big) == 8
+    assert ef.library().ef_status_string(13) != b"unknown status"
 
 
 @needs_lib
