@@ -23,6 +23,10 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG, "_build")
 LIB_DIR = os.path.join(PKG, "lib")
 LIB_PATH = os.path.join(LIB_DIR, "libef_attention.so")
+# Microbenchmarks of the measurement script (streaming read, bare matrix-core
+# loop): a library of their own, so the attention library exports only its ABI.
+MICRO_DIR = os.path.join(CSRC, "micro")
+MICRO_LIB_PATH = os.path.join(LIB_DIR, "libef_micro.so")
 
 ARCH = "gfx950"
 HIP_FLAGS = [
@@ -59,26 +63,33 @@ def _run(cmd, verbose):
         print(err, flush=True)
 
 
+def _link(cc, objs, path, verbose):
+    tmp = path + ".tmp"
+    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
+    os.replace(tmp, path)
+
+
 def build(verbose: bool = False) -> str:
-    """Compile every csrc/*.hip for gfx950 and link lib/libef_attention.so; returns its path."""
+    """Compile every csrc/*.hip for gfx950 and link lib/libef_attention.so (and the
+    microbenchmarks of csrc/micro/ into lib/libef_micro.so); returns the first path."""
     os.makedirs(BUILD_DIR, exist_ok=True)
     os.makedirs(LIB_DIR, exist_ok=True)
     cc = hipcc()
     sources = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+    micro = sorted(glob.glob(os.path.join(MICRO_DIR, "*.hip")))
     if not sources:
         raise RuntimeError("no HIP sources found")
-    objs = []
-    jobs = []
-    with cf.ThreadPoolExecutor(max_workers=min(8, len(sources))) as ex:
-        for src in sources:
+    objs, micro_objs, jobs = [], [], []
+    with cf.ThreadPoolExecutor(max_workers=min(8, len(sources) + len(micro))) as ex:
+        for src in sources + micro:
             obj = os.path.join(BUILD_DIR, os.path.basename(src)[:-4] + ".o")
-            objs.append(obj)
+            (micro_objs if src in micro else objs).append(obj)
             jobs.append(ex.submit(_run, [cc, *HIP_FLAGS, "-c", src, "-o", obj], verbose))
         for j in jobs:
             j.result()
-    tmp = LIB_PATH + ".tmp"
-    _run([cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp], verbose)
-    os.replace(tmp, LIB_PATH)
+    _link(cc, objs, LIB_PATH, verbose)
+    if micro_objs:
+        _link(cc, micro_objs, MICRO_LIB_PATH, verbose)
     return LIB_PATH
 
 

@@ -107,6 +107,89 @@ def traffic(fetch_csv, write_csv, kernel_substr):
     }
 
 
+# Counter passes of the matrix-core profile (each within the per-pass limits of the
+# hardware: at most 8 SQ counters, GRBM counters apart).
+COUNTER_PASSES = (
+    ("SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_BUSY_CYCLES", "SQ_WAIT_INST_ANY", "SQ_WAIT_ANY",
+     "SQ_INSTS_VALU", "SQ_INSTS_LDS", "GRBM_GUI_ACTIVE"),
+    ("SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_ACTIVE_INST_VALU",
+     "SQ_ACTIVE_INST_LDS", "SQ_LDS_BANK_CONFLICT", "SQ_WAIT_INST_LDS", "SQ_INSTS_SALU",
+     "SQ_ACTIVE_INST_ANY"),
+    ("SQ_INSTS_MFMA", "SQ_LDS_IDX_ACTIVE", "SQ_INSTS_VALU_TRANS_F32", "SQ_ACTIVE_INST_MISC",
+     "SQ_INSTS_BRANCH"),
+)
+XCDS = 8
+SIMDS = 1024  # 256 compute units x 4 SIMDs
+
+
+def counter_summary(paths, kernel_substr, avg_us, algorithmic_flops=None):
+    """Per-dispatch means of the counters of the kernel over the given counter CSVs, and
+    what they imply: the clock (GRBM_GUI_ACTIVE counts every XCD's busy cycles), the
+    matrix-core busy fraction of all SIMD cycles, the matrix flops actually issued
+    (SQ_INSTS_VALU_MFMA_MOPS_BF16 counts units of 512 flops) and instruction mixes."""
+    acc = defaultdict(list)
+    kname = None
+    for path in paths:
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if kernel_substr in r["Kernel_Name"]:
+                    kname = r["Kernel_Name"]
+                    acc[r["Counter_Name"]].append(float(r["Counter_Value"]))
+    d = {k: sum(v) / len(v) for k, v in acc.items()}
+    out = {"kernel": kname, "means": d}
+    if "GRBM_GUI_ACTIVE" in d and avg_us:
+        cyc = d["GRBM_GUI_ACTIVE"] / XCDS
+        out["clock_mhz"] = cyc / avg_us
+        if "SQ_VALU_MFMA_BUSY_CYCLES" in d:
+            out["mfma_busy_frac"] = d["SQ_VALU_MFMA_BUSY_CYCLES"] / (cyc * SIMDS)
+        if "SQ_BUSY_CYCLES" in d:
+            out["sq_busy_frac"] = d["SQ_BUSY_CYCLES"] / (cyc * XCDS)
+    if "SQ_INSTS_VALU_MFMA_MOPS_BF16" in d:
+        out["mfma_flops"] = d["SQ_INSTS_VALU_MFMA_MOPS_BF16"] * 512.0
+        if algorithmic_flops:
+            out["mfma_flops_over_algorithmic"] = out["mfma_flops"] / algorithmic_flops
+    w = d.get("SQ_WAVES")
+    if w:
+        out["per_wave"] = {k: v / w for k, v in d.items() if k.startswith("SQ_INSTS")}
+        if "SQ_INSTS_MFMA" in d:
+            out["valu_per_mfma"] = d.get("SQ_INSTS_VALU", 0.0) / d["SQ_INSTS_MFMA"]
+    if "SQ_WAVE_CYCLES" in d and "SQ_WAIT_INST_ANY" in d:
+        out["wait_inst_frac"] = d["SQ_WAIT_INST_ANY"] / d["SQ_WAVE_CYCLES"]
+    if "SQ_LDS_IDX_ACTIVE" in d and "SQ_LDS_BANK_CONFLICT" in d:
+        out["lds_bank_conflict_frac"] = d["SQ_LDS_BANK_CONFLICT"] / max(d["SQ_LDS_IDX_ACTIVE"], 1)
+    return out
+
+
+def counter_lines(c, algorithmic_flops=None):
+    lines = ["", "## Matrix-core counters (rocprofv3 --pmc, three passes)", ""]
+    if "clock_mhz" in c:
+        lines.append(f"- clock while the kernel runs: {c['clock_mhz']:.0f} MHz "
+                     f"(GRBM_GUI_ACTIVE / {XCDS} XCDs / average duration)")
+    if "mfma_busy_frac" in c:
+        lines.append(f"- matrix core busy: {100 * c['mfma_busy_frac']:.1f}% of all SIMD cycles "
+                     f"(SQ_VALU_MFMA_BUSY_CYCLES / (cycles x {SIMDS} SIMDs))")
+    if "mfma_flops" in c:
+        extra = (f", {c['mfma_flops_over_algorithmic']:.3f} x the algorithmic "
+                 f"{algorithmic_flops / 1e9:.1f} GFLOP (masked tiles computed whole)"
+                 if "mfma_flops_over_algorithmic" in c else "")
+        lines.append(f"- matrix flops issued: {c['mfma_flops'] / 1e9:.1f} GFLOP per dispatch "
+                     f"(SQ_INSTS_VALU_MFMA_MOPS_BF16 x 512){extra}")
+    if "valu_per_mfma" in c:
+        lines.append(f"- vector instructions per matrix instruction: {c['valu_per_mfma']:.2f}")
+    if "wait_inst_frac" in c:
+        lines.append(f"- waves waiting on an instruction dependency: "
+                     f"{100 * c['wait_inst_frac']:.1f}% of wave cycles")
+    if "lds_bank_conflict_frac" in c:
+        lines.append(f"- LDS bank conflicts: {100 * c['lds_bank_conflict_frac']:.2f}% of LDS "
+                     f"active cycles")
+    lines += ["", "| counter | per dispatch | per wave |", "|---|---|---|"]
+    w = c["means"].get("SQ_WAVES") or 0
+    for k in sorted(c["means"]):
+        v = c["means"][k]
+        lines.append(f"| {k} | {v:.4g} | {v / w:.4g} |" if w else f"| {k} | {v:.4g} | |")
+    return lines
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--stats", required=True)
@@ -118,6 +201,9 @@ def main():
     ap.add_argument("--algorithmic-bytes", type=float, default=None)
     ap.add_argument("--command", required=True, help="the rocprofv3 command lines that were run")
     ap.add_argument("--bench-line", default=None, help="file holding the bench JSON line")
+    ap.add_argument("--counters", nargs="*", default=None,
+                    help="counter_collection CSVs of the matrix-core counter passes")
+    ap.add_argument("--algorithmic-flops", type=float, default=None)
     ap.add_argument("--out-prefix", required=True)
     a = ap.parse_args()
 
@@ -127,7 +213,8 @@ def main():
              "## rocprofv3 --kernel-trace --stats", "",
              "| kernel | calls | avg us | min us | max us | % time |", "|---|---|---|---|---|---|"]
     for s in stats:
-        lines.append(f"| `{s['name']}` | {s['calls']} | {s['avg_us']:.2f} | {s['min_us']:.2f} | "
+        name = s["name"] if len(s["name"]) <= 120 else s["name"][:117] + "..."
+        lines.append(f"| `{name}` | {s['calls']} | {s['avg_us']:.2f} | {s['min_us']:.2f} | "
                      f"{s['max_us']:.2f} | {s['pct']:.1f} |")
     if a.fetch and a.write:
         t = traffic(a.fetch, a.write, a.kernel)
@@ -153,6 +240,13 @@ def main():
                   "", f"Source hash of {', '.join(a.sources)}: `{t['source_hash']}`."]
         with open(a.out_prefix + "_traffic.json", "w") as f:
             json.dump(t, f, indent=1)
+    if a.counters:
+        avg = next((st["avg_us"] for st in stats if a.kernel in st["name"]), None)
+        c = counter_summary(a.counters, a.kernel, avg, a.algorithmic_flops)
+        lines += counter_lines(c, a.algorithmic_flops)
+        lines += ["", f"Source hash of {', '.join(a.sources)}: `{source_hash(*a.sources)}`."]
+        with open(a.out_prefix + "_counters.json", "w") as f:
+            json.dump({**c, "source_hash": source_hash(*a.sources), "avg_us": avg}, f, indent=1)
     if a.bench_line:
         with open(a.bench_line) as f:
             js = [ln for ln in f if ln.startswith("{")]
