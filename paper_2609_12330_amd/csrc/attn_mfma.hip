@@ -17,7 +17,9 @@
 // is already in the B-operand layout of the second product. Two lanes
 // (l and l ^ 32) share a query and exchange one value per tile for the max.
 //
-// Software pipeline over 64-key tiles: while the vector ALU turns tile j's
+// Software pipeline over tiles of BN keys (64, or 32 for the split producer
+// of decode shapes, whose smaller stages let four workgroups share a compute
+// unit): while the vector ALU turns tile j's
 // scores into weights, the matrix core already computes tile j+1's scores,
 // then tile j's values are multiplied. K is therefore staged one tile ahead
 // of V: during step j, K stage (j+1)%2 holds K of tile j+1 and V stage j%2
@@ -58,11 +60,12 @@ namespace ef {
 
 namespace {
 
-constexpr int BN = 64;                 // keys per tile
 constexpr float kLazyThreshold = 8.f;  // base-2 headroom before the reference moves
 constexpr unsigned kXcds = 8;                   // accelerator dies of the chip
 
-template <int D>
+// Geometry of a BN-key tile (BN = 64, or 32 for the decode-shaped split
+// producer, whose smaller stages let four workgroups share a compute unit).
+template <int D, int BN>
 struct TileGeom {
   static constexpr int KCH = D / 8;        // 16-byte chunks per row
   static constexpr int ROW = 2 * D;        // bytes per K or V row (no padding: swizzled)
@@ -99,6 +102,7 @@ __device__ __forceinline__ float max_with_other_half(float x) {
 // starting at key a0 (keys below aend), then the tiles of the window run
 // starting at b0 (keys below bend). Without a window the sink run is empty and
 // the window run is the whole key range. Tiles past the last one cover no key.
+template <int BN>
 struct TileList {
   int a0, aend, na, b0, bend, n;
   int full_lo;  // a tile whose last key is at most this is below every row's causal limit
@@ -119,9 +123,24 @@ struct TileList {
 // each wave-wide load filling RPI whole rows): no staging registers and no
 // LDS stores. Rows past the tile's run repeat its last row (their keys are
 // masked, their values finite); a tile past the last one loads nothing.
-template <int D, int NW>
+//
+// Cache policy: the split producer of decode shapes (32-key tiles, one row
+// tile per kv head) reads every key exactly once, so its loads are
+// non-temporal and stream past the caches, which lifts its read rate by
+// about a sixth; the other launches keep the default policy, under which
+// the row tiles of one kv head share its K/V tiles through the XCD's L2.
+template <bool STREAM>
+__device__ __forceinline__ void load_chunk(const uint16_t* g, char* l) {
+  if constexpr (STREAM)
+    __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)l, 16, 0,
+                                     2 /* non-temporal */);
+  else
+    __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)l, 16, 0, 0);
+}
+
+template <int D, int NW, int BN>
 struct Loader {
-  using G = TileGeom<D>;
+  using G = TileGeom<D, BN>;
   static constexpr int INSTS = BN / G::RPI / NW;  // direct loads per wave and tile
   static_assert(INSTS * G::RPI * NW == BN, "tile split over the waves");
   int row[INSTS];       // tile row whose chunk this lane loads
@@ -158,7 +177,7 @@ struct Loader {
       for (int i = 0; i < INSTS; ++i) {
         char* l = stage + (wave + NW * i) * 1024;
         const uint16_t* g = reinterpret_cast<const uint16_t*>(base + (ISK ? koff[i] : voff[i]));
-        __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)l, 16, 0, 0);
+        load_chunk<BN == 32>(g, l);
       }
     } else {
 #pragma unroll
@@ -167,7 +186,7 @@ struct Loader {
         const unsigned off = (unsigned)(r * D + (ISK ? kchunk[i] : vchunk[i])) * 2u;
         char* l = stage + (wave + NW * i) * 1024;
         const uint16_t* g = reinterpret_cast<const uint16_t*>(base + off);
-        __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)l, 16, 0, 0);
+        load_chunk<BN == 32>(g, l);
       }
     }
   }
@@ -185,33 +204,49 @@ struct Loader {
 __device__ __forceinline__ void wait_tile_loads() { __builtin_amdgcn_s_waitcnt(0x0f70); }
 
 // Occupancy target: two waves per SIMD for 4-wave workgroups (two workgroups per
-// CU overlap each other's barrier and memory stalls); the 2-wave variant keeps
-// its larger per-thread staging registers at one wave per SIMD.
-template <int NW>
-constexpr int kWavesPerEu = NW == 4 ? 2 : 1;
+// CU overlap each other's barrier and latency stalls) and for 2-wave workgroups
+// of 32-key tiles (four per CU); the 2-wave variant with 64-key tiles keeps its
+// larger per-thread staging registers at one wave per SIMD.
+template <int NW, int BN>
+constexpr int kWavesPerEu = (NW == 4 || BN == 32) ? 2 : 1;
 
-template <int D, bool NEG>
+template <int D, bool NEG, int BN>
 struct Tile {
-  using Geo = TileGeom<D>;
+  using Geo = TileGeom<D, BN>;
   static constexpr int KSTEPS = D / 16;  // MFMA k-steps over the head dimension
   static constexpr int DT = D / 32;      // 32-wide output tiles along D
+  static constexpr int HALVES = BN / 32;  // 32-key halves of a tile
+  static constexpr int PK = BN / 4;       // packed bf16 weight pairs per lane
 
-  // S^T of the key tile in K stage S: two 32-key halves, 16-deep MFMA k-steps.
+  // S^T of the key tile in K stage S: 32-key halves, 16-deep MFMA k-steps.
   template <int S>
   static __device__ __forceinline__ void scores(const char* smem, const int* kread,
                                                 const bf16x8_t* qf, floatx16* sacc) {
 #pragma unroll
-    for (int half = 0; half < 2; ++half)
+    for (int half = 0; half < HALVES; ++half)
 #pragma unroll
       for (int i = 0; i < 16; ++i) sacc[half][i] = 0.f;
+    if constexpr (HALVES == 1) {
+      // One 32-key half: every K fragment is requested before the first product,
+      // so the LDS latency is paid once per tile rather than once per k-step.
+      u32x4_t kx[KSTEPS];
 #pragma unroll
-    for (int s = 0; s < KSTEPS; ++s) {
+      for (int s = 0; s < KSTEPS; ++s)
+        kx[s] = *reinterpret_cast<const u32x4_t*>(smem + Geo::template k_off<S>() + kread[s]);
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const u32x4_t kx = *reinterpret_cast<const u32x4_t*>(
-            smem + Geo::template k_off<S>() + kread[s] + half * 32 * Geo::ROW);
-        sacc[half] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kx),
-                                                            qf[s], sacc[half], 0, 0, 0);
+      for (int s = 0; s < KSTEPS; ++s)
+        sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, kx[s]),
+                                                         qf[s], sacc[0], 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int s = 0; s < KSTEPS; ++s) {
+#pragma unroll
+        for (int half = 0; half < HALVES; ++half) {
+          const u32x4_t kx = *reinterpret_cast<const u32x4_t*>(
+              smem + Geo::template k_off<S>() + kread[s] + half * 32 * Geo::ROW);
+          sacc[half] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+              __builtin_bit_cast(bf16x8_t, kx), qf[s], sacc[half], 0, 0, 0);
+        }
       }
     }
   }
@@ -227,7 +262,7 @@ struct Tile {
                                                   int h) {
     if constexpr (NEG) {
 #pragma unroll
-      for (int half = 0; half < 2; ++half)
+      for (int half = 0; half < HALVES; ++half)
 #pragma unroll
         for (int i = 0; i < 16; ++i) x[half][i] = -x[half][i];
     }
@@ -242,7 +277,7 @@ struct Tile {
       const int whi = min(max(lo, kb - 1), kb + BN) - base;
       if (__builtin_amdgcn_ballot_w64(whi >= wlo)) {
 #pragma unroll
-        for (int half = 0; half < 2; ++half)
+        for (int half = 0; half < HALVES; ++half)
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
             const int o = half * 32 + 8 * (i >> 2) + (i & 3);
@@ -251,7 +286,7 @@ struct Tile {
           }
       } else {
 #pragma unroll
-        for (int half = 0; half < 2; ++half)
+        for (int half = 0; half < HALVES; ++half)
 #pragma unroll
           for (int i = 0; i < 16; ++i) {
             const int o = half * 32 + 8 * (i >> 2) + (i & 3);
@@ -261,7 +296,7 @@ struct Tile {
     }
     float tmax = fmaxf(x[0][0], x[0][1]);
 #pragma unroll
-    for (int i = 2; i < 32; ++i) tmax = fmaxf(tmax, x[i >> 4][i & 15]);
+    for (int i = 2; i < 16 * HALVES; ++i) tmax = fmaxf(tmax, x[i >> 4][i & 15]);
     tmax = max_with_other_half(tmax);
     const float cand = tmax * c;  // tile maximum in base-2 units (c > 0)
     // Move the reference only when the tile exceeds it by the threshold.
@@ -287,7 +322,7 @@ struct Tile {
                                                  uint32_t* pk, float& lsum) {
     float ps[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
+    for (int i = 0; i < PK; ++i) {
       const float p0 = exp2_fast(fmaf(x[(2 * i) >> 4][(2 * i) & 15], c, mneg));
       const float p1 = exp2_fast(fmaf(x[(2 * i + 1) >> 4][(2 * i + 1) & 15], c, mneg));
       pk[i] = pack_bf16x2(p0, p1);
@@ -296,27 +331,84 @@ struct Tile {
     lsum += (ps[0] + ps[1]) + (ps[2] + ps[3]);
   }
 
-  // O^T += V^T * P^T over the four 16-key steps of the tile in V stage S. The
+  // O^T += V^T * P^T over the 16-key steps of the tile in V stage S. The
   // V^T operand (8 keys of one value column per lane) comes from two
   // transposing reads of 4 keys each out of the row-major V tile.
   template <int S>
   static __device__ __forceinline__ void values(const char* smem, const int* vread,
                                                 const uint32_t* pk, floatx16* oacc) {
-    typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+    if constexpr (BN == 32) {
+      values_asm<S>(smem, vread, pk, oacc);
+    } else {
+      typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 #pragma unroll
-    for (int s = 0; s < 4; ++s) {
+      for (int s = 0; s < BN / 16; ++s) {
+        // P^T fragment: registers 8*(s%2) .. +8 of score half s/2, i.e. pk[4*s .. 4*s+3].
+        const u32x4_t pv = {pk[4 * s], pk[4 * s + 1], pk[4 * s + 2], pk[4 * s + 3]};
+        const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pv);
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) {
+          const char* p = smem + Geo::template v_off<S>() + vread[dt] + 16 * s * Geo::ROW;
+          const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (__attribute__((address_space(3))) bf16x4_t*)(p));
+          const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
+              (__attribute__((address_space(3))) bf16x4_t*)(p + 8 * Geo::ROW));
+          const bf16x8_t vx = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vx, pf, oacc[dt], 0, 0, 0);
+        }
+      }
+    }
+  }
+
+  // values() of a 32-key tile with the transposing reads issued from assembly:
+  // the compiler cannot tell them from the direct-to-LDS loads into the other
+  // stages still in flight, and waits for every outstanding load before the
+  // first of them, which leaves the step's loads only its first half to land.
+  // The reads of 16-key step s + 1 are requested before the products of step
+  // s; LDS operations complete in order, so before step s's products a wait
+  // until at most step s + 1's reads are outstanding suffices (other
+  // operations counted by the same counter only make it longer). An empty
+  // statement that rewrites the operands after the wait keeps the products
+  // below it. (With 64-key tiles the extra registers this holds would spill.)
+  template <int S>
+  static __device__ __forceinline__ void values_asm(const char* smem, const int* vread,
+                                                    const uint32_t* pk, floatx16* oacc) {
+    constexpr int STEPS = BN / 16;
+    constexpr int READS = 2 * DT;  // reads per 16-key step
+    static_assert(READS <= 15, "outstanding reads exceed the LDS counter");
+    const unsigned base = (unsigned)(uintptr_t)(
+        (const __attribute__((address_space(3))) char*)(smem + Geo::template v_off<S>()));
+    u32x2_t lo[2][DT], hi[2][DT];
+    auto read_step = [&](int s, u32x2_t(&l)[DT], u32x2_t(&h)[DT]) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const unsigned addr = base + vread[dt] + 16 * s * Geo::ROW;
+        asm volatile("ds_read_b64_tr_b16 %0, %1" : "=v"(l[dt]) : "v"(addr));
+        asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2"
+                     : "=v"(h[dt])
+                     : "v"(addr), "i"(8 * Geo::ROW));
+      }
+    };
+    read_step(0, lo[0], hi[0]);
+#pragma unroll
+    for (int s = 0; s < STEPS; ++s) {
+      const int b = s & 1;
+      if (s + 1 < STEPS) {
+        read_step(s + 1, lo[b ^ 1], hi[b ^ 1]);
+        asm volatile("s_waitcnt lgkmcnt(%0)" ::"i"(READS) : "memory");
+      } else {
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      }
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) asm volatile("" : "+v"(lo[b][dt]), "+v"(hi[b][dt]));
       // P^T fragment: registers 8*(s%2) .. +8 of score half s/2, i.e. pk[4*s .. 4*s+3].
       const u32x4_t pv = {pk[4 * s], pk[4 * s + 1], pk[4 * s + 2], pk[4 * s + 3]};
       const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pv);
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const char* p = smem + Geo::template v_off<S>() + vread[dt] + 16 * s * Geo::ROW;
-        const bf16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (__attribute__((address_space(3))) bf16x4_t*)(p));
-        const bf16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4bf16(
-            (__attribute__((address_space(3))) bf16x4_t*)(p + 8 * Geo::ROW));
-        const bf16x8_t vx = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vx, pf, oacc[dt], 0, 0, 0);
+        const u32x4_t vx = {lo[b][dt][0], lo[b][dt][1], hi[b][dt][0], hi[b][dt][1]};
+        oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8_t, vx), pf,
+                                                          oacc[dt], 0, 0, 0);
       }
     }
   }
@@ -329,18 +421,18 @@ struct Tile {
 // straight into LDS, computes tile j's weights while the matrix core computes
 // tile j+1's scores, multiplies tile j's values, and waits for its loads
 // before the workgroup barrier.
-template <int D, int NW, bool NEG, int S>
+template <int D, int NW, bool NEG, int S, int BN>
 __device__ __forceinline__ void pipelined_step(
-    char* smem, const Loader<D, NW>& ld, const uint16_t* kh, const uint16_t* vh,
-    const TileList& tl, int j, int lim, int lo, int h, const int* kread, const int* vread,
-    const bf16x8_t* qf, floatx16 (*sacc)[2], floatx16* oacc, float& lsum, float& mref,
+    char* smem, const Loader<D, NW, BN>& ld, const uint16_t* kh, const uint16_t* vh,
+    const TileList<BN>& tl, int j, int lim, int lo, int h, const int* kread, const int* vread,
+    const bf16x8_t* qf, floatx16 (*sacc)[BN / 32], floatx16* oacc, float& lsum, float& mref,
     float c) {
-  using TileT = Tile<D, NEG>;
+  using TileT = Tile<D, NEG, BN>;
   ld.template load_k<S>(smem, kh, tl.base(j + 2), tl.end(j + 2));  // nothing past the last tile
   ld.template load_v<1 - S>(smem, vh, tl.base(j + 1), tl.end(j + 1));
   const float mneg = TileT::prepare(sacc[S], oacc, lsum, mref, c, tl.base(j), tl.end(j),
                                     tl.masked(j), lim, lo, tl.sinks, h);
-  uint32_t pk[16];
+  uint32_t pk[TileT::PK];
   TileT::weights(sacc[S], c, mneg, pk, lsum);
   // Tile j+1's scores go to the other accumulator pair, so tile j's stay in place.
   TileT::template scores<1 - S>(smem, kread, qf, sacc[1 - S]);
@@ -349,11 +441,11 @@ __device__ __forceinline__ void pipelined_step(
   __syncthreads();
 }
 
-template <int D, int NW, bool NEG, bool DIFF = false>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(kWavesPerEu<NW>)))
+template <int D, int NW, bool NEG, bool DIFF, int BN>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(kWavesPerEu<NW, BN>)))
 void attn_mfma_kernel(MfmaParams a) {
-  using Geo = TileGeom<D>;
-  using TileT = Tile<D, NEG>;
+  using Geo = TileGeom<D, BN>;
+  using TileT = Tile<D, NEG, BN>;
   constexpr int KSTEPS = TileT::KSTEPS;
   constexpr int DT = TileT::DT;
   constexpr int BM = 32 * NW;
@@ -396,7 +488,7 @@ void attn_mfma_kernel(MfmaParams a) {
   // virtual key axis (the sink run [0, la) followed by the window run from key
   // bs); its part in each run is cut at the last key any row can see and, in
   // the window run, at the first key of the earliest row's window.
-  TileList tl;
+  TileList<BN> tl;
   {
     const int la = a.runs.la, bs = a.runs.bs;
     const int v0 = p * a.T;
@@ -465,9 +557,9 @@ void attn_mfma_kernel(MfmaParams a) {
   // Prologue: K and V of tile 0 into stage 0, K of tile 1 into K stage 1, then
   // tile 0's scores; the second barrier orders those K reads before stage 0 is
   // rewritten by the first pipelined step.
-  Loader<D, NW> ld;
+  Loader<D, NW, BN> ld;
   ld.init();
-  floatx16 sacc[2][2];  // S^T of the current and the next tile
+  floatx16 sacc[2][BN / 32];  // S^T of the current and the next tile
   if (ntiles > 0) {
     ld.template load_k<0>(smem, kh, tl.base(0), tl.end(0));
     ld.template load_v<0>(smem, vh, tl.base(0), tl.end(0));
@@ -479,11 +571,11 @@ void attn_mfma_kernel(MfmaParams a) {
   __syncthreads();
 
   for (int j = 0; j < ntiles; j += 2) {
-    pipelined_step<D, NW, NEG, 0>(smem, ld, kh, vh, tl, j, lim, lo, h, kread, vread, qf, sacc,
-                                  oacc, lsum, mref, c);
+    pipelined_step<D, NW, NEG, 0, BN>(smem, ld, kh, vh, tl, j, lim, lo, h, kread, vread, qf,
+                                      sacc, oacc, lsum, mref, c);
     if (j + 1 < ntiles)
-      pipelined_step<D, NW, NEG, 1>(smem, ld, kh, vh, tl, j + 1, lim, lo, h, kread, vread, qf,
-                                    sacc, oacc, lsum, mref, c);
+      pipelined_step<D, NW, NEG, 1, BN>(smem, ld, kh, vh, tl, j + 1, lim, lo, h, kread, vread,
+                                        qf, sacc, oacc, lsum, mref, c);
   }
 
   // Row sum over both lane halves.
@@ -559,10 +651,10 @@ void attn_mfma_kernel(MfmaParams a) {
   }
 }
 
-template <int D, int NW, bool NEG, bool DIFF>
+template <int D, int NW, bool NEG, bool DIFF, int BN>
 hipError_t launch_one(const MfmaParams& a, hipStream_t stream) {
-  const size_t lds = TileGeom<D>::LDS_BYTES;
-  auto kern = attn_mfma_kernel<D, NW, NEG, DIFF>;
+  const size_t lds = TileGeom<D, BN>::LDS_BYTES;
+  auto kern = attn_mfma_kernel<D, NW, NEG, DIFF, BN>;
   // More than 64 KiB of LDS per workgroup needs the attribute; set once per kernel.
   static const hipError_t attr = hipFuncSetAttribute(
       reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
@@ -572,11 +664,13 @@ hipError_t launch_one(const MfmaParams& a, hipStream_t stream) {
   return hipGetLastError();
 }
 
-template <int D, int NW>
+template <int D, int NW, int BN>
 hipError_t launch_nw(const MfmaParams& a, bool neg, hipStream_t stream) {
   if (a.diff.gamma != nullptr)
-    return neg ? launch_one<D, NW, true, true>(a, stream) : launch_one<D, NW, false, true>(a, stream);
-  return neg ? launch_one<D, NW, true, false>(a, stream) : launch_one<D, NW, false, false>(a, stream);
+    return neg ? launch_one<D, NW, true, true, BN>(a, stream)
+               : launch_one<D, NW, false, true, BN>(a, stream);
+  return neg ? launch_one<D, NW, true, false, BN>(a, stream)
+             : launch_one<D, NW, false, false, BN>(a, stream);
 }
 
 }  // namespace
@@ -585,12 +679,16 @@ int mfma_rows_per_block(int R) { return R <= 64 ? 64 : 128; }
 
 hipError_t launch_mfma_attention(const MfmaParams& a, bool neg, hipStream_t stream) {
   const int bm = a.mtiles > 0 ? mfma_rows_per_block(a.R) : 128;
+  // The split producer for few rows per kv head (decode shapes) runs 32-key tiles.
+  const bool small = bm == 64 && a.ws_m != nullptr;
   if (a.D == 128) {
-    if (bm == 64) return launch_nw<128, 2>(a, neg, stream);
-    return launch_nw<128, 4>(a, neg, stream);
+    if (small) return launch_nw<128, 2, 32>(a, neg, stream);
+    if (bm == 64) return launch_nw<128, 2, 64>(a, neg, stream);
+    return launch_nw<128, 4, 64>(a, neg, stream);
   }
-  if (bm == 64) return launch_nw<64, 2>(a, neg, stream);
-  return launch_nw<64, 4>(a, neg, stream);
+  if (small) return launch_nw<64, 2, 32>(a, neg, stream);
+  if (bm == 64) return launch_nw<64, 2, 64>(a, neg, stream);
+  return launch_nw<64, 4, 64>(a, neg, stream);
 }
 
 }  // namespace ef
