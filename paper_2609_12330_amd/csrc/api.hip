@@ -105,6 +105,36 @@ constexpr double kFusedCombineUsPer16 = 4.4;
 constexpr double kCombineValuUs = 8.9;
 constexpr double kCombineMfmaUs = 13.4;
 
+// Rows per workgroup of the matrix-core kernel (section 6.2). The legal
+// schedules hold 64 or 128 query rows of one kv head (two or four waves of 32
+// rows). Each is charged an optimistic time, the larger of its matrix work over
+// the bf16 peak and its global-memory traffic over the HBM peak, and the
+// fastest is taken; with equal times, the one with less matrix work. Matrix
+// work counts the rows padded to whole workgroups; traffic counts the K/V that
+// every row tile stages (each re-read in full: the L2 is not credited) plus q
+// and o once. `keys`: the keys a row tile streams.
+constexpr double kMfmaPeakFlopsPerUs = 2.5e9;
+constexpr double kHbmPeakBytesPerUs = 8.0e6;
+
+int rows_per_block(const Shape& s, double keys) {
+  const double R = (double)(s.Hq / s.Hkv) * s.Sq;
+  const double kv_heads = (double)s.B * s.Hkv;
+  int best = 0;
+  double best_us = 0.0, best_flops = 0.0;
+  for (const int bm : {64, 128}) {
+    const double tiles = std::ceil(R / bm);
+    const double flops = kv_heads * tiles * bm * keys * 4.0 * s.D;
+    const double bytes = kv_heads * tiles * keys * 4.0 * s.D + (double)s.rows() * s.D * 6.0;
+    const double us = std::max(flops / kMfmaPeakFlopsPerUs, bytes / kHbmPeakBytesPerUs);
+    if (best == 0 || us < best_us || (us == best_us && flops < best_flops)) {
+      best = bm;
+      best_us = us;
+      best_flops = flops;
+    }
+  }
+  return best;
+}
+
 double split_model_us(const Shape& s, int keys, int T, int visible) {
   const int G = s.Hq / s.Hkv;
   const int R = G * s.Sq;
@@ -120,7 +150,7 @@ double split_model_us(const Shape& s, int keys, int T, int visible) {
     wg_per_part = 1;
     wg_rate = kWgValuBytesPerUs[bucket];
   } else {
-    const int bm = ef::mfma_rows_per_block(R);
+    const int bm = rows_per_block(s, std::min<double>(T, visible));
     nw = bm / 32;
     wg_per_part = std::ceil((double)R / bm);
     wg_rate = kWaveMfmaBytesPerUs * nw;
@@ -176,7 +206,7 @@ int visible_keys(const Shape& s, const ef::KeyRuns& runs) {
   const int R = G * s.Sq;
   const int pos = R <= kDecodeValuRows
                       ? s.Sq
-                      : std::min(s.Sq, (ef::mfma_rows_per_block(R) + G - 1) / G);
+                      : std::min(s.Sq, (rows_per_block(s, runs.lv) + G - 1) / G);
   const long long v = (long long)runs.window + runs.sinks + pos;
   return (int)std::min<long long>(runs.lv, v);
 }
@@ -246,8 +276,8 @@ ef_status launch_mfma(const Shape& s, const void* q, const void* k, const void* 
   a.R = a.G * s.Sq;
   a.T = T;
   a.P = P;
-  const int bm = ef::mfma_rows_per_block(a.R);
-  a.mtiles = (a.R + bm - 1) / bm;
+  a.bm = rows_per_block(s, std::min(T, runs.lv));
+  a.mtiles = (a.R + a.bm - 1) / a.bm;
   a.c_abs = std::fabs(scale) * ef::kLog2e;
   a.causal = causal ? 1 : 0;
   a.runs = runs;

@@ -675,12 +675,12 @@ hipError_t launch_nw(const MfmaParams& a, bool neg, hipStream_t stream) {
 
 }  // namespace
 
-int mfma_rows_per_block(int R) { return R <= 64 ? 64 : 128; }
-
 hipError_t launch_mfma_attention(const MfmaParams& a, bool neg, hipStream_t stream) {
-  const int bm = a.mtiles > 0 ? mfma_rows_per_block(a.R) : 128;
-  // The split producer for few rows per kv head (decode shapes) runs 32-key tiles.
-  const bool small = bm == 64 && a.ws_m != nullptr;
+  const int bm = a.bm;
+  if (bm != 64 && bm != 128) return hipErrorInvalidValue;
+  // The split producer with one row tile per kv head (decode shapes) runs
+  // 32-key tiles, whose non-temporal loads assume every key is read once.
+  const bool small = bm == 64 && a.mtiles == 1 && a.ws_m != nullptr;
   if (a.D == 128) {
     if (small) return launch_nw<128, 2, 32>(a, neg, stream);
     if (bm == 64) return launch_nw<128, 2, 64>(a, neg, stream);

@@ -79,6 +79,7 @@ struct MfmaParams {
   int B, Hq, Hkv, Sq, Skv, D;
   int G, R;
   int T, P;      // keys per partition and partitions (T >= Skv, P = 1 in single-pass mode)
+  int bm;        // query rows per workgroup: 64 (two waves) or 128 (four)
   int mtiles;    // query-row tiles per kv head
   float c_abs;   // |scale| * log2(e)
   int causal;
@@ -106,7 +107,5 @@ hipError_t launch_decode_split(const DecodeParams& a, hipStream_t stream);
 hipError_t launch_mfma_attention(const MfmaParams& a, bool negative_scale, hipStream_t stream);
 hipError_t launch_combine(const CombineParams& a, hipStream_t stream);
 
-// Rows per workgroup of the MFMA kernel for a problem with R rows per kv head.
-int mfma_rows_per_block(int R);
 
 }  // namespace ef
