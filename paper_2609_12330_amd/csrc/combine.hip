@@ -4,14 +4,13 @@
 //
 // Two layouts. With few partitions (P <= 32) one wave takes a whole row, each
 // lane owning D/64 adjacent elements and folding the partitions in order. With
-// many partitions, one wave takes a (row, 8-element slice of D): lane l takes partitions
-// p = l/2, l/2 + 32, ... and one 4-float half of the slice, so each pass of the
-// wave reads 32 partitions x 32 contiguous bytes and every lane keeps several
-// independent loads in flight. Each lane folds its partitions into one state
-// with the same reducer (reference moves up to the larger maximum, the other
-// side is rescaled by exp of the difference; the identity state (-inf, 0, 0)
-// contributes nothing), then the 32 partition lanes of each half merge
-// pairwise in a fixed butterfly order, so the result is deterministic.
+// many partitions, a workgroup takes a (row, 16-element slice of D) and
+// requests up to 512 partitions' values at once; each lane folds its
+// partitions into one state with the same reducer (reference moves up to the
+// larger maximum, the other side is rescaled by exp of the difference; the
+// identity state (-inf, 0, 0) contributes nothing), then the lanes merge in a
+// fixed butterfly order and the waves in a fixed order, so the result is
+// deterministic.
 #include "diff_norm.hpp"
 #include "ef_device.hpp"
 #include "ef_kernels.hpp"
@@ -20,9 +19,6 @@ namespace ef {
 
 namespace {
 
-constexpr int kSlice = 8;              // floats of D per wave
-constexpr int kLanesPerPart = kSlice / 4;  // lanes per partition (one float4 each)
-constexpr int kPartsPerPass = 64 / kLanesPerPart;
 constexpr int kRowsKernelMaxP = 32;  // up to this many partitions: one wave per row
 
 struct Acc4 {
@@ -46,39 +42,79 @@ __device__ __forceinline__ void fold(Acc4& s, float mb, float lb, float b0, floa
 
 }  // namespace
 
-// Many partitions: one wave per (row, 8-float slice).
-__global__ __launch_bounds__(64) void combine_sliced_kernel(CombineParams a) {
-  const int lane = threadIdx.x;
-  const int slices = a.D / kSlice;
+// Many partitions, in one round trip: one workgroup of four waves per (row,
+// 16-float slice of D). Four adjacent lanes read a partition's 64 contiguous
+// bytes of the slice, so a pass of the workgroup covers 64 partitions, and the
+// eight passes of 512 partitions are all requested before any is folded. Each
+// lane folds its partitions in order with the reducer; the 16 partition lanes
+// of each quarter in a wave merge by butterfly, then the four waves' states in
+// order through LDS, so the result is deterministic.
+constexpr int kWideSlice = 16;                         // floats of D per workgroup
+constexpr int kWideLanes = kWideSlice / 4;             // lanes per partition (a float4 each)
+constexpr int kWideThreads = 256;
+constexpr int kWideGroups = kWideThreads / kWideLanes;  // partitions per pass
+constexpr int kWidePasses = 8;                         // passes in flight
+
+__global__ __launch_bounds__(kWideThreads) void combine_wide_kernel(CombineParams a) {
+  const int slices = a.D / kWideSlice;
   const int row = blockIdx.x / slices;
   const int slice = blockIdx.x % slices;
   const int P = a.P;
-  const int half = lane % kLanesPerPart;
-  const int p0 = lane / kLanesPerPart;
+  const int t = threadIdx.x;
+  const int quarter = t % kWideLanes;
+  const int g = t / kWideLanes;
   const float* mrow = a.m + (size_t)row * P;
   const float* lrow = a.l + (size_t)row * P;
-  const float* arow = a.acc + (size_t)row * P * a.D + slice * kSlice + half * 4;
+  const float* arow = a.acc + (size_t)row * P * a.D + slice * kWideSlice + quarter * 4;
 
   Acc4 s{kNegInf, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-  for (int p = p0; p < P; p += kPartsPerPass) {
-    const float mp = mrow[p];
-    const float lp = lrow[p];
-    const float4 x = *reinterpret_cast<const float4*>(arow + (size_t)p * a.D);
-    fold(s, mp, lp, x.x, x.y, x.z, x.w);
+  for (int p0 = 0; p0 < P; p0 += kWideGroups * kWidePasses) {
+    float mv[kWidePasses], lv[kWidePasses];
+    float4 x[kWidePasses];
+    // Unconditional reads of a clamped partition (a guarded read compiles to a
+    // branch); a partition past the last folds as the identity state.
+#pragma unroll
+    for (int i = 0; i < kWidePasses; ++i) {
+      const int pc = min(p0 + g + kWideGroups * i, P - 1);
+      mv[i] = mrow[pc];
+      lv[i] = lrow[pc];
+      x[i] = *reinterpret_cast<const float4*>(arow + (size_t)pc * a.D);
+    }
+#pragma unroll
+    for (int i = 0; i < kWidePasses; ++i) {
+      const bool in = p0 + g + kWideGroups * i < P;
+      fold(s, in ? mv[i] : kNegInf, in ? lv[i] : 0.f, in ? x[i].x : 0.f, in ? x[i].y : 0.f,
+           in ? x[i].z : 0.f, in ? x[i].w : 0.f);
+    }
   }
 #pragma unroll
-  for (int off = kLanesPerPart; off < 64; off <<= 1) {
+  for (int off = kWideLanes; off < 64; off <<= 1) {
     const float mb = shfl_xor(s.m, off), lb = shfl_xor(s.l, off);
     const float b0 = shfl_xor(s.a0, off), b1 = shfl_xor(s.a1, off);
     const float b2 = shfl_xor(s.a2, off), b3 = shfl_xor(s.a3, off);
     fold(s, mb, lb, b0, b1, b2, b3);
   }
-  if (lane < kLanesPerPart) {
-    const bool empty = s.m == kNegInf || s.l == 0.f;
-    const float inv = empty ? 0.f : 1.f / s.l;
-    float4 out = make_float4(s.a0 * inv, s.a1 * inv, s.a2 * inv, s.a3 * inv);
-    *reinterpret_cast<float4*>(a.o + (size_t)row * a.D + slice * kSlice + half * 4) = out;
+  constexpr int kWaves = kWideThreads / 64;
+  __shared__ float st[kWaves][kWideLanes][6];
+  const int wave = t / 64, lane = t % 64;
+  if (lane < kWideLanes) {
+    st[wave][lane][0] = s.m;
+    st[wave][lane][1] = s.l;
+    st[wave][lane][2] = s.a0;
+    st[wave][lane][3] = s.a1;
+    st[wave][lane][4] = s.a2;
+    st[wave][lane][5] = s.a3;
+  }
+  __syncthreads();
+  if (t < kWideLanes) {
+    Acc4 r{st[0][t][0], st[0][t][1], st[0][t][2], st[0][t][3], st[0][t][4], st[0][t][5]};
+#pragma unroll
+    for (int w = 1; w < kWaves; ++w)
+      fold(r, st[w][t][0], st[w][t][1], st[w][t][2], st[w][t][3], st[w][t][4], st[w][t][5]);
+    const bool empty = r.m == kNegInf || r.l == 0.f;
+    const float inv = empty ? 0.f : 1.f / r.l;
+    *reinterpret_cast<float4*>(a.o + (size_t)row * a.D + slice * kWideSlice + t * 4) =
+        make_float4(r.a0 * inv, r.a1 * inv, r.a2 * inv, r.a3 * inv);
   }
 }
 
@@ -146,8 +182,9 @@ hipError_t launch_combine(const CombineParams& a, hipStream_t stream) {
                            : (diff ? combine_rows_kernel<64, true> : combine_rows_kernel<64, false>);
     hipLaunchKernelGGL(kern, dim3(blocks), dim3(256), 0, stream, a);
   } else {
-    const size_t waves = (size_t)a.rows * (a.D / kSlice);
-    hipLaunchKernelGGL(combine_sliced_kernel, dim3((unsigned)waves), dim3(64), 0, stream, a);
+    const size_t blocks = (size_t)a.rows * (a.D / kWideSlice);
+    hipLaunchKernelGGL(combine_wide_kernel, dim3((unsigned)blocks), dim3(kWideThreads), 0,
+                       stream, a);
   }
   return hipGetLastError();
 }
