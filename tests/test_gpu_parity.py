@@ -262,7 +262,9 @@ def test_config_prefill_split_matches_fwd():
 # ---------------------------------------------------------------------------
 
 
-@pytest.mark.parametrize("P", [1, 2, 16, 512, 513])
+# P <= 32 takes the one-wave-per-row layout; above, the wide layout, which requests
+# 512 partitions per round (33: its smallest; 513, 1100: a ragged second or third round).
+@pytest.mark.parametrize("P", [1, 2, 16, 32, 33, 512, 513, 1100])
 @pytest.mark.parametrize("D", [64, 128])
 def test_combine_fp32(P, D):
     announce(f"combine P={P} D={D}")
