@@ -227,8 +227,9 @@ struct Tile {
 #pragma unroll
       for (int i = 0; i < 16; ++i) sacc[half][i] = 0.f;
     if constexpr (HALVES == 1) {
-      // One 32-key half: every K fragment is requested before the first product,
-      // so the LDS latency is paid once per tile rather than once per k-step.
+      // One 32-key half: each K fragment has registers of its own, so the reads
+      // can run several products ahead (the compiler issues them in two
+      // batches) rather than one product ahead.
       u32x4_t kx[KSTEPS];
 #pragma unroll
       for (int s = 0; s < KSTEPS; ++s)
