@@ -246,6 +246,20 @@ double ef_attention_splitkv_modeled_us(int B, int Hq, int Hkv, int Sq, int Skv, 
                                        int window, int sinks, int partition_size);
 
 /*
+ * Query rows per workgroup of the matrix-core kernel for these sizes, as the
+ * entry points choose them (64 or 128; the Hq/Hkv query heads of a kv head
+ * are packed into its rows). The choice follows the roofline rule of section
+ * 6.2 over the legal values: each is charged the larger of its matrix work
+ * (rows padded to whole workgroups) over the bf16 peak and its global-memory
+ * traffic (the K/V that every row tile stages, plus q and o) over the HBM
+ * peak; the smallest wins, and with equal times the one with less matrix
+ * work. `keys`: the keys a row tile streams (Skv for a full or causal
+ * prefill, the partition size in a split-KV call). Returns 0 for invalid
+ * sizes or keys < 0.
+ */
+int ef_attention_rows_per_workgroup(int B, int Hq, int Hkv, int Sq, int Skv, int D, int keys);
+
+/*
  * Measures the best partition size for these inputs on this device: the six
  * candidates the model rates fastest (among those whose workspace fits in
  * workspace_bytes) are timed by successive halving (section 6.3: every

@@ -577,6 +577,12 @@ double ef_attention_splitkv_modeled_us(int B, int Hq, int Hkv, int Sq, int Skv, 
   return split_model_us(s, runs.lv, partition_size, visible_keys(s, runs));
 }
 
+int ef_attention_rows_per_workgroup(int B, int Hq, int Hkv, int Sq, int Skv, int D, int keys) {
+  const Shape s{B, Hq, Hkv, Sq, Skv, D};
+  if (check_shape(s) != EF_OK || keys < 0) return 0;
+  return rows_per_block(s, keys);
+}
+
 ef_status ef_attention_splitkv_tune(const void* q, const void* k, const void* v, float* o, int B,
                                     int Hq, int Hkv, int Sq, int Skv, int D, float scale,
                                     int causal, int window, int sinks, void* workspace,

@@ -57,6 +57,7 @@ SIGNATURES = {
     "ef_attention_splitkv_local_partition_size": (_i, [_i, _i, _i, _i, _i, _i, _i, _i, _i]),
     "ef_attention_splitkv_local_workspace_size": (_sz, [_i, _i, _i, _i, _i, _i, _i, _i, _i]),
     "ef_attention_splitkv_modeled_us": (ctypes.c_double, [_i, _i, _i, _i, _i, _i, _i, _i, _i]),
+    "ef_attention_rows_per_workgroup": (_i, [_i, _i, _i, _i, _i, _i, _i]),
     "ef_attention_splitkv_tune": (_i, [_vp, _vp, _vp, _fp, _i, _i, _i, _i, _i, _i, _f, _i, _i, _i,
                                        _vp, _sz, _vp, ctypes.POINTER(ctypes.c_int)]),
     "ef_diff_attention": (_i, [_vp, _vp, _vp, _vp, _vp, _fp, _fp, _fp, _fp, _fp, _fp, _f, _f, _i,
@@ -200,6 +201,10 @@ def ef_attention_splitkv_local_workspace_size(B, Hq, Hkv, Sq, Skv, D, window, si
 def ef_attention_splitkv_modeled_us(B, Hq, Hkv, Sq, Skv, D, window, sinks, partition_size) -> float:
     return _lib().ef_attention_splitkv_modeled_us(B, Hq, Hkv, Sq, Skv, D, window, sinks,
                                                   partition_size)
+
+
+def ef_attention_rows_per_workgroup(B, Hq, Hkv, Sq, Skv, D, keys) -> int:
+    return _lib().ef_attention_rows_per_workgroup(B, Hq, Hkv, Sq, Skv, D, keys)
 
 
 def ef_attention_splitkv_tune(q, k, v, o, B, Hq, Hkv, Sq, Skv, D, scale, causal, window, sinks,

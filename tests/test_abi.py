@@ -339,6 +339,28 @@ def test_local_workspace_and_partition_arithmetic():
 
 
 @needs_lib
+def test_rows_per_workgroup_choice():
+    """Rows per workgroup of the matrix-core kernel by the roofline rule over 64 and 128 rows:
+    a row tile of 128 rows stages each K/V tile once for twice the rows, so it wins whenever
+    it needs fewer row tiles (more than 64 rows per kv head); at 64 rows or fewer both need
+    one and the padding to 128 rows doubles the matrix work, so 64 wins."""
+    rpw = ef.ef_attention_rows_per_workgroup
+    assert rpw(4, 32, 8, 2048, 2048, 128, 2048) == 128   # causal GQA prefill, 8192 rows per kv head
+    assert rpw(16, 64, 8, 8, 8192, 128, 2048) == 64      # chunked decode, 64 rows per kv head
+    assert rpw(1, 8, 1, 8, 2000, 128, 64) == 64
+    assert rpw(1, 4, 4, 64, 64, 64, 64) == 64            # tiny MHA
+    for G, Sq in [(1, 1), (4, 1), (8, 8), (2, 32), (1, 64), (8, 9), (4, 17), (1, 65), (2, 33),
+                  (16, 8), (1, 129), (3, 50), (8, 2048)]:
+        for keys in (64, 2048, 131072):
+            want = 64 if G * Sq <= 64 else 128
+            assert rpw(2, 8 * G, 8, Sq, keys, 128, keys) == want, (G, Sq, keys)
+            assert rpw(2, 8 * G, 8, Sq, keys, 64, keys) == want, (G, Sq, keys)
+    assert rpw(1, 3, 2, 8, 64, 128, 64) == 0             # Hq not a multiple of Hkv
+    assert rpw(1, 4, 2, 8, 64, 96, 64) == 0              # unsupported head dimension
+    assert rpw(1, 4, 2, 8, 64, 128, -1) == 0
+
+
+@needs_lib
 def test_roofline_partition_choice():
     """partition_size = 0 takes the candidate the roofline model rates fastest. On MI355X the
     picks below were the measured best of 64, 128, ..., 8192 keys per partition (or within 3%
