@@ -499,8 +499,8 @@ def measure(cfg, args, ef, wl, torch, dev, seed, cpu_budget, clock=None):
 
 def micro(torch, dev):
     """Achievable ceilings on this part at its running clock: a streaming read over a
-    rotating 2 GiB buffer (slices of the GQA decode's 134 MB, and whole 1 GiB reads) and
-    a bare v_mfma_f32_32x32x16_bf16 loop."""
+    rotating 2 GiB buffer (slices of the GQA decode's 134 MB and of the long and chunked
+    decodes' 537 MB, and whole 1 GiB reads) and a bare v_mfma_f32_32x32x16_bf16 loop."""
     from paper_2609_12330_amd import build as b
 
     if not os.path.exists(b.MICRO_LIB_PATH):
@@ -514,7 +514,8 @@ def micro(torch, dev):
     buf = torch.empty(total, dtype=torch.uint8, device=dev).fill_(1)
     sink = torch.empty(256 * 64, dtype=torch.int32, device=dev)
     stream = torch.cuda.current_stream()
-    for label, nbytes in (("read_134MB_slices", 134414336), ("read_1GiB", 1 << 30)):
+    for label, nbytes in (("read_134MB_slices", 134414336), ("read_537MB_slices", 536870912),
+                          ("read_1GiB", 1 << 30)):
         n_slices = total // nbytes
         reps = 64 if nbytes < (1 << 28) else 8
         sweep = {}
