@@ -442,6 +442,36 @@ def test_graph_capture_replays_match_eager():
         assert torch.equal(o_fwd, e_fwd), f"replay {rep}: fwd differs from eager"
 
 
+@pytest.mark.parametrize("D", [128, 64])
+def test_largest_key_extent(D):
+    """The largest key count the ABI accepts: Skv * D just below 2^31 elements per kv head
+    (16.8M keys at D = 128, 33.6M at D = 64), so byte offsets inside a head come within
+    2 * D bytes of 2^32. The single pass (one workgroup streams every key) and split-KV
+    (library partitions) against the oracle, whose reference combines per-chunk partial
+    states with its own combine (the split form, pinned equal to the definition)."""
+    Skv = (1 << 31) // D - 1
+    B, Hq, Hkv, Sq = 1, 4, 1, 1
+    announce(f"largest key extent Skv={Skv} D={D}")
+    q, k, v = wl.make_device_inputs(B, Hq, Hkv, Sq, Skv, D, seed=31, device="cuda")
+    scale = 1.0 / math.sqrt(D)
+    o_fwd = ef.attention_fwd(q, k, v, scale=scale)
+    o_split = ef.attention_splitkv(q, k, v, scale=scale)
+    torch.cuda.synchronize()
+    q64 = wl.to_f64(q.cpu())
+    chunk = 1 << 20
+    states = []
+    for s in range(0, Skv, chunk):
+        e = min(s + chunk, Skv)
+        states.append(oracle.splitkv_partials_ref(q64, wl.to_f64(k[:, :, s:e].cpu()),
+                                                  wl.to_f64(v[:, :, s:e].cpu()), scale, False,
+                                                  partition_size=e - s))
+    m, l, acc = (np.concatenate([st[i] for st in states], axis=1) for i in range(3))
+    ref = oracle.combine_ref(m, l, acc).reshape(B, Hq, Sq, D)
+    assert_close(o_fwd, ref, "largest key extent fwd")
+    assert_close(o_split, ref, "largest key extent splitkv")
+    assert ef.ef_attention_splitkv_workspace_size(B, Hq, Hkv, Sq, Skv + 1, D, 0) == 0
+
+
 @pytest.mark.parametrize("shape", [(8, 32, 8, 1, 4096, 128, 256), (2, 8, 2, 2, 1000, 128, 64),
                                    (1, 32, 8, 1, 70000, 128, 2048)],
                          ids=lambda s: "x".join(map(str, s)))
