@@ -109,3 +109,21 @@ def test_diff_workload_and_inputs():
     assert gamma.dtype == torch.float32 and gamma.shape == (64,)
     assert torch.equal(q1, b[0]) and torch.equal(v, b[4]) and torch.equal(gamma, b[6])
     assert not torch.equal(q1, q2) and not torch.equal(k1, k2)
+
+
+def test_device_inputs_are_seeded_bf16_draws():
+    """The device-side generator of the largest-extent tests: deterministic per seed, bf16
+    values of N(0,1) draws (rounded from fp32), chunked draws filling every key row."""
+    a = wl.make_device_inputs(1, 4, 2, 1, 1000, 64, seed=5, device="cpu", chunk_rows=300)
+    b = wl.make_device_inputs(1, 4, 2, 1, 1000, 64, seed=5, device="cpu", chunk_rows=300)
+    c = wl.make_device_inputs(1, 4, 2, 1, 1000, 64, seed=6, device="cpu", chunk_rows=300)
+    for x, y in zip(a, b):
+        assert x.dtype == torch.bfloat16 and torch.equal(x, y)
+    assert not torch.equal(a[1], c[1])
+    q, k, v = a
+    assert q.shape == (1, 4, 1, 64) and k.shape == v.shape == (1, 2, 1000, 64)
+    for t in (k, v):
+        f = t.float()
+        assert abs(float(f.mean())) < 0.05 and abs(float(f.std()) - 1.0) < 0.05
+        assert (f.abs().sum(dim=-1) > 0).all()  # no row left unwritten
+
