@@ -182,24 +182,22 @@ def make_shape_inputs(B, Hq, Hkv, Sq, Skv, D, seed, q_mult=1.0):
 
 def make_device_inputs(B, Hq, Hkv, Sq, Skv, D, seed, device, chunk_rows=1 << 20):
     """Inputs drawn on `device` with a seeded generator of that device, for shapes whose
-    host-side draw would take minutes (the largest key extents): q [B,Hq,Sq,D] and
-    k, v [B,Hkv,Skv,D] as bf16(N(0,1)), each drawn in fp32 and rounded to bf16 (RNE)
-    `chunk_rows` key rows at a time. A different stream of numbers from
-    :func:`make_shape_inputs` for the same seed."""
+    host-side draw would take minutes (the largest extents the ABI accepts): q [B,Hq,Sq,D]
+    and k, v [B,Hkv,Skv,D] as bf16(N(0,1)), in that order, each drawn in fp32 and rounded
+    to bf16 (RNE) `chunk_rows` rows (of D elements, in memory order) at a time. A different
+    stream of numbers from :func:`make_shape_inputs` for the same seed."""
     g = torch.Generator(device=device)
     g.manual_seed(int(seed))
-    q = torch.randn(B, Hq, Sq, D, generator=g, device=device).to(torch.bfloat16)
-    out = []
-    for _ in range(2):
-        t = torch.empty(B, Hkv, Skv, D, dtype=torch.bfloat16, device=device)
-        for b in range(B):
-            for h in range(Hkv):
-                for s in range(0, Skv, chunk_rows):
-                    e = min(s + chunk_rows, Skv)
-                    t[b, h, s:e] = torch.randn(e - s, D, generator=g, device=device).to(
-                        torch.bfloat16)
-        out.append(t)
-    return q, out[0], out[1]
+
+    def draw(*shape):
+        t = torch.empty(*shape, dtype=torch.bfloat16, device=device)
+        flat = t.view(-1, D)
+        for s in range(0, flat.shape[0], chunk_rows):
+            e = min(s + chunk_rows, flat.shape[0])
+            flat[s:e] = torch.randn(e - s, D, generator=g, device=device).to(torch.bfloat16)
+        return t
+
+    return draw(B, Hq, Sq, D), draw(B, Hkv, Skv, D), draw(B, Hkv, Skv, D)
 
 
 # Differential attention constants of the synthetic layer: the mixing weight's

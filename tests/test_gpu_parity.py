@@ -472,6 +472,47 @@ def test_largest_key_extent(D):
     assert ef.ef_attention_splitkv_workspace_size(B, Hq, Hkv, Sq, Skv + 1, D, 0) == 0
 
 
+def test_largest_query_extent():
+    """The largest query count the ABI accepts at D = 128 (Sq * D just below 2^31 elements
+    per head: 16.8M query rows, 131,072 row tiles in the grid), over 100 keys, through the
+    single pass. The oracle checks sampled rows, the last ones included (rows are
+    independent without a causal mask)."""
+    D = 128
+    Sq = (1 << 31) // D - 1
+    B, Hq, Hkv, Skv = 1, 1, 1, 100
+    announce(f"largest query extent Sq={Sq}")
+    q, k, v = wl.make_device_inputs(B, Hq, Hkv, Sq, Skv, D, seed=32, device="cuda")
+    scale = 1.0 / math.sqrt(D)
+    o = ef.attention_fwd(q, k, v, scale=scale)
+    torch.cuda.synchronize()
+    rows = sorted({0, 1, 127, 128, Sq // 2, Sq - 129, Sq - 128, Sq - 2, Sq - 1} |
+                  set(range(Sq - 64, Sq)))
+    idx = torch.tensor(rows, device="cuda")
+    ref = oracle.attention_ref(wl.to_f64(q[:, :, idx].cpu()), wl.to_f64(k.cpu()),
+                               wl.to_f64(v.cpu()), scale, False)
+    assert_close(o[:, :, idx], ref, "largest query extent fwd")
+    assert np.isfinite(o[0, 0, ::4096].cpu().numpy()).all()
+
+
+def test_largest_kv_head_grid():
+    """B * Hkv at the grid limit the ABI accepts (65,535 kv heads): single pass and split-KV
+    (fused combine: more groups than counter slots, so the combine kernel runs) on sampled
+    batch rows, the first and the last ones included."""
+    B, Hq, Hkv, Sq, Skv, D = 65535, 2, 1, 1, 70, 64
+    announce("largest kv-head grid")
+    q, k, v = wl.make_device_inputs(B, Hq, Hkv, Sq, Skv, D, seed=33, device="cuda")
+    scale = 1.0 / math.sqrt(D)
+    o_fwd = ef.attention_fwd(q, k, v, scale=scale)
+    o_split = ef.attention_splitkv(q, k, v, scale=scale, partition_size=64)
+    torch.cuda.synchronize()
+    bs = torch.tensor([0, 1, 2, 511, 512, 32767, 65022, 65533, 65534], device="cuda")
+    ref = oracle.attention_ref(wl.to_f64(q[bs].cpu()), wl.to_f64(k[bs].cpu()),
+                               wl.to_f64(v[bs].cpu()), scale, False)
+    assert_close(o_fwd[bs], ref, "largest kv-head grid fwd")
+    assert_close(o_split[bs], ref, "largest kv-head grid splitkv")
+    assert ef.ef_attention_splitkv_workspace_size(B + 1, Hq, Hkv, Sq, Skv, D, 64) == 0
+
+
 @pytest.mark.parametrize("shape", [(8, 32, 8, 1, 4096, 128, 256), (2, 8, 2, 2, 1000, 128, 64),
                                    (1, 32, 8, 1, 70000, 128, 2048)],
                          ids=lambda s: "x".join(map(str, s)))
