@@ -330,10 +330,14 @@ ef_status fwd_impl(const Shape& s, const void* q, const void* k, const void* v, 
                      hs);
 }
 
+// The split-KV entry points reject more partitions than the grid takes; the
+// size queries report such arguments as invalid (0) too.
 int partition_size_impl(const Shape& s, const ef::KeyRuns& runs, int partition_size) {
   if (check_shape(s) != EF_OK) return 0;
   if (partition_size < 0 || partition_size % kTileKeys != 0) return 0;
-  return resolve_partition(s, runs.lv, partition_size, visible_keys(s, runs));
+  const int T = resolve_partition(s, runs.lv, partition_size, visible_keys(s, runs));
+  if ((runs.lv + (long long)T - 1) / T > kMaxGridYZ) return 0;
+  return T;
 }
 
 size_t workspace_size_impl(const Shape& s, const ef::KeyRuns& runs, int partition_size) {
@@ -342,6 +346,7 @@ size_t workspace_size_impl(const Shape& s, const ef::KeyRuns& runs, int partitio
   if (s.rows() == 0 || s.Skv == 0) return 0;
   const int T = resolve_partition(s, runs.lv, partition_size, visible_keys(s, runs));
   const long long P = (runs.lv + (long long)T - 1) / T;
+  if (P > kMaxGridYZ) return 0;
   return ws_layout(s.rows(), P, s.D).bytes;
 }
 
@@ -748,7 +753,7 @@ size_t ef_diff_attention_workspace_size(int B, int Hq, int Hkv, int Sq, int Skv,
   const Shape s{B, Hq, Hkv, Sq, Skv, D};
   int T = 0;
   const long long P = diff_partitions(s, partition_size, &T);
-  if (P <= 1) return 0;
+  if (P <= 1 || P > kMaxGridYZ) return 0;
   return ws_layout(s.rows(), P, s.D).bytes;
 }
 

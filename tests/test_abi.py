@@ -339,6 +339,22 @@ def test_local_workspace_and_partition_arithmetic():
 
 
 @needs_lib
+def test_size_queries_reject_too_many_partitions():
+    """The split-KV entry points take at most 65,535 partitions (the grid's limit); the
+    size queries report one more as invalid (0), as they do for any other invalid argument."""
+    ws = ef.ef_attention_splitkv_workspace_size
+    ps = ef.ef_attention_splitkv_partition_size
+    edge = 65535 * 64
+    assert ws(1, 4, 1, 1, edge, 128, 64) > 0 and ps(1, 4, 1, 1, edge, 128, 64) == 64
+    assert ws(1, 4, 1, 1, edge + 1, 128, 64) == 0 and ps(1, 4, 1, 1, edge + 1, 128, 64) == 0
+    assert ps(1, 4, 1, 1, edge + 1, 128, 0) > 64  # the library's own choice stays valid
+    assert ef.ef_attention_splitkv_local_workspace_size(1, 4, 1, 1, edge + 1, 128, edge, 0,
+                                                        64) == 0
+    assert ef.ef_diff_attention_workspace_size(1, 4, 1, 1, edge, 128, 64) > 0
+    assert ef.ef_diff_attention_workspace_size(1, 4, 1, 1, edge + 1, 128, 64) == 0
+
+
+@needs_lib
 def test_rows_per_workgroup_choice():
     """Rows per workgroup of the matrix-core kernel by the roofline rule over 64 and 128 rows:
     a row tile of 128 rows stages each K/V tile once for twice the rows, so it wins whenever

@@ -472,6 +472,33 @@ def test_largest_key_extent(D):
     assert ef.ef_attention_splitkv_workspace_size(B, Hq, Hkv, Sq, Skv + 1, D, 0) == 0
 
 
+@pytest.mark.parametrize("Hq", [4, 8], ids=["vector_producer", "matrix_core_producer"])
+def test_largest_partition_count(Hq):
+    """65,535 partitions of 64 keys, the most the ABI accepts, on one kv head (4 or 8 query
+    rows): the producer's partition axis at the grid limit and the combine kernel over
+    65,535 states per row (128 rounds of its 512-partition batches)."""
+    B, Hkv, Sq, D, T = 1, 1, 1, 128, 64
+    Skv = 65535 * T
+    announce(f"largest partition count Hq={Hq}")
+    q, k, v = wl.make_device_inputs(B, Hq, Hkv, Sq, Skv, D, seed=34, device="cuda")
+    scale = 1.0 / math.sqrt(D)
+    assert ef.splitkv_partitions(Sq, Skv, T) == 65535
+    o = ef.attention_splitkv(q, k, v, scale=scale, partition_size=T)
+    torch.cuda.synchronize()
+    q64 = wl.to_f64(q.cpu())
+    chunk = 1 << 20
+    states = []
+    for s in range(0, Skv, chunk):
+        e = min(s + chunk, Skv)
+        states.append(oracle.splitkv_partials_ref(q64, wl.to_f64(k[:, :, s:e].cpu()),
+                                                  wl.to_f64(v[:, :, s:e].cpu()), scale, False,
+                                                  partition_size=e - s))
+    m, l, acc = (np.concatenate([st[i] for st in states], axis=1) for i in range(3))
+    assert_close(o, oracle.combine_ref(m, l, acc).reshape(B, Hq, Sq, D),
+                 f"largest partition count Hq={Hq}")
+    assert ef.ef_attention_splitkv_workspace_size(B, Hq, Hkv, Sq, Skv + 1, D, T) == 0
+
+
 def test_largest_query_extent():
     """The largest query count the ABI accepts at D = 128 (Sq * D just below 2^31 elements
     per head: 16.8M query rows, 131,072 row tiles in the grid), over 100 keys, through the
