@@ -536,7 +536,10 @@ void attn_mfma_kernel(MfmaParams a) {
     for (int j = 0; j < 16; ++j) oacc[i][j] = 0.f;
   float mref = kNegInf;  // reference maximum, base-2 units
   float lsum = 0.f;      // this lane's half of the row sum
-  const float c = a.c_abs;
+  // The floor keeps a zero scale well defined: every visible key gets weight 1
+  // (2^(x c) rounds to 1 for any finite score), while a hidden key's -inf stays
+  // -inf instead of becoming -inf * 0 = NaN.
+  const float c = fmaxf(a.c_abs, 1e-30f);
   // Per-lane LDS byte offsets of the fragment reads inside a stage: K row ql,
   // chunk 2s + h of k-step s; and, per 32-column tile dt of V^T, the
   // transposing-read pointer of this lane (row 4(lane/32) + (lane%16)/4 of a

@@ -400,6 +400,57 @@ def test_empty_inputs():
     assert (o[:, :, :2] == 0).all() and torch.isfinite(o).all()
 
 
+@pytest.mark.parametrize("shape", [(1, 2, 1, 2, 1, 128, 64),    # 4 rows: vector producer
+                                   (2, 8, 1, 8, 5, 128, 64),    # 64 rows: matrix-core producer
+                                   (1, 32, 1, 12, 7, 64, 64)],  # 384 rows: three row tiles
+                         ids=lambda s: "x".join(map(str, s)))
+def test_split_causal_rows_that_see_nothing(shape):
+    """Causal split-KV with Sq > Skv: the first Sq - Skv query positions see no key and must
+    come out 0 (their partial states are the reducer identity in every partition)."""
+    B, Hq, Hkv, Sq, Skv, D, T = shape
+    announce(f"split rows that see nothing {shape}")
+    q, k, v = inputs(B, Hq, Hkv, Sq, Skv, D, seed=17)
+    o = run_split(q, k, v, 1 / math.sqrt(D), True, T)
+    torch.cuda.synchronize()
+    ref = oracle.attention_ref(f64(q), f64(k), f64(v), 1 / math.sqrt(D), True)
+    assert_close(o, ref, f"split causal Sq > Skv {shape}")
+    assert (o[:, :, :Sq - Skv] == 0).all()
+
+
+@pytest.mark.parametrize("path", ["fwd", "splitkv"])
+def test_zero_scale_averages_visible_values(path):
+    """scale = 0: every visible key weighs the same, so each output row is the plain mean
+    of the value rows it sees (closed form, no oracle)."""
+    announce(f"zero scale {path}")
+    B, Hq, Hkv, Sq, Skv, D = 1, 8, 2, 5, 700, 128
+    q, k, v = inputs(B, Hq, Hkv, Sq, Skv, D, seed=18)
+    o = run_fwd(q, k, v, 0.0, True) if path == "fwd" else run_split(q, k, v, 0.0, True, 128)
+    torch.cuda.synchronize()
+    v64 = f64(v)
+    G = Hq // Hkv
+    want = np.zeros((B, Hq, Sq, D))
+    for hq in range(Hq):
+        for i in range(Sq):
+            last = i + Skv - Sq  # bottom-right causal: keys 0 .. last are visible
+            want[0, hq, i] = v64[0, hq // G, :last + 1].mean(axis=0)
+    assert_close(o, want, f"zero scale {path}")
+
+
+@pytest.mark.parametrize("shape", [(2, 32, 1, 1, 1000, 128, 256),  # MQA decode, 32 rows
+                                   (1, 64, 1, 4, 500, 64, 128),    # 256 rows, two row tiles
+                                   (1, 16, 1, 1, 3000, 128, 0)],   # 16 rows, library partitions
+                         ids=lambda s: "x".join(map(str, s)))
+def test_multi_query_attention(shape):
+    """One kv head for all query heads (GQA ratios 16 to 64), single pass and split-KV."""
+    B, Hq, Hkv, Sq, Skv, D, T = shape
+    announce(f"MQA {shape}")
+    q, k, v = inputs(B, Hq, Hkv, Sq, Skv, D, seed=19)
+    scale = 1 / math.sqrt(D)
+    ref = oracle.attention_ref(f64(q), f64(k), f64(v), scale, True)
+    assert_close(run_fwd(q, k, v, scale, True), ref, f"MQA fwd {shape}")
+    assert_close(run_split(q, k, v, scale, True, T), ref, f"MQA split {shape}")
+
+
 def test_non_default_stream():
     announce("stream")
     q, k, v = inputs(1, 8, 2, 1, 2048, 128, seed=13)
