@@ -22,13 +22,16 @@
  *     bf16 is the IEEE binary32 upper half (1-8-7). All pointers are DEVICE
  *     pointers, 16-byte aligned; the caller owns every buffer and keeps it
  *     alive until the stream has passed the call. The library allocates
- *     nothing and keeps no state between calls; calls are thread-safe.
+ *     nothing and keeps no state between calls (apart from the static scratch
+ *     of ef_attention_splitkv_noalloc); calls are thread-safe.
  *   - D must be 64 or 128. Hq and Hkv must be >= 1 with Hq % Hkv == 0.
  *     B, Sq and Skv may be 0: with B*Hq*Sq == 0 nothing is written, with
  *     Skv == 0 every output row is 0. Per head, S*D must stay below 2^31.
  *   - causal != 0 applies a bottom-right aligned mask: key j is visible to
  *     query i iff j <= i + (Skv - Sq). A query row that sees no key gets 0.
- *   - scale multiplies the fp32-accumulated q.k products; it must be finite.
+ *   - scale multiplies the fp32-accumulated q.k products; it must be finite
+ *     (0 gives every visible key the same weight). The scaled scores are fp32
+ *     values: |scale * q.k| beyond the fp32 range is outside the contract.
  *   - Every call validates its arguments on the host, synchronously, before
  *     anything is enqueued. On an error nothing is launched and no buffer is
  *     written. After validation the work is enqueued on `stream` (a
@@ -62,7 +65,8 @@ typedef enum {
   EF_ERR_GQA_RATIO = 3,            /* Hq is not a multiple of Hkv */
   EF_ERR_UNSUPPORTED_HEAD_DIM = 4, /* D is not 64 or 128 */
   EF_ERR_MISALIGNED = 5,           /* a pointer is not 16-byte aligned */
-  EF_ERR_INVALID_PARTITION = 6,    /* partition_size is not 0 or a positive multiple of 64 */
+  EF_ERR_INVALID_PARTITION = 6,    /* partition_size is not 0 or a positive multiple of 64, or
+                                      it gives more than 65535 partitions */
   EF_ERR_WORKSPACE_TOO_SMALL = 7,  /* workspace is NULL or smaller than required */
   EF_ERR_INVALID_SCALE = 8,        /* scale is NaN or infinite */
   EF_ERR_HIP = 9,                  /* HIP reported an error when the work was enqueued */
