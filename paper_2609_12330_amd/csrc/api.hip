@@ -299,7 +299,9 @@ const char* ef_status_string(int status) {
     case EF_ERR_GQA_RATIO: return "Hq is not a multiple of Hkv";
     case EF_ERR_UNSUPPORTED_HEAD_DIM: return "head dimension must be 64 or 128";
     case EF_ERR_MISALIGNED: return "a pointer is not 16-byte aligned";
-    case EF_ERR_INVALID_PARTITION: return "partition_size must be 0 or a positive multiple of 64";
+    case EF_ERR_INVALID_PARTITION:
+      return "partition_size must be 0 or a positive multiple of 64 giving at most 65535 "
+             "partitions";
     case EF_ERR_WORKSPACE_TOO_SMALL: return "workspace is NULL or too small";
     case EF_ERR_INVALID_SCALE: return "scale is not finite";
     case EF_ERR_HIP: return "HIP error while enqueueing work";
