@@ -52,6 +52,8 @@
 // y = A1 - lambda * A2 from the carried value, mixes in lambda from the four
 // learned vectors, RMS-normalises the row over D (the two lanes of a query
 // hold its two halves) and writes the result, so A1 never reaches HBM.
+#include <atomic>
+
 #include "diff_norm.hpp"
 #include "ef_device.hpp"
 #include "ef_kernels.hpp"
@@ -659,10 +661,20 @@ template <int D, int NW, bool NEG, bool DIFF, int BN>
 hipError_t launch_one(const MfmaParams& a, hipStream_t stream) {
   const size_t lds = TileGeom<D, BN>::LDS_BYTES;
   auto kern = attn_mfma_kernel<D, NW, NEG, DIFF, BN>;
-  // More than 64 KiB of LDS per workgroup needs the attribute; set once per kernel.
-  static const hipError_t attr = hipFuncSetAttribute(
-      reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (attr != hipSuccess) return attr;
+  // More than 64 KiB of LDS per workgroup needs the attribute, which belongs to
+  // the kernel on one device: set once per device (ids below 64 are
+  // remembered, higher ones set it on every launch).
+  static std::atomic<unsigned long long> lds_set{0};
+  int dev = 0;
+  const hipError_t de = hipGetDevice(&dev);
+  if (de != hipSuccess) return de;
+  const unsigned long long bit = (dev >= 0 && dev < 64) ? 1ull << dev : 0ull;
+  if (bit == 0 || (lds_set.load(std::memory_order_acquire) & bit) == 0) {
+    const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (attr != hipSuccess) return attr;
+    lds_set.fetch_or(bit, std::memory_order_acq_rel);
+  }
   dim3 grid(a.mtiles, a.P, a.B * a.Hkv);
   hipLaunchKernelGGL(kern, grid, dim3(NW * 64), lds, stream, a);
   return hipGetLastError();
