@@ -67,6 +67,17 @@ __device__ __forceinline__ void reset_counter(unsigned* counter) {
   __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// Lanes that form one row of the weights pass, and the maximum over each such
+// aligned group of 16 lanes (every lane gets it).
+constexpr int kRowLanes = 16;
+__device__ __forceinline__ float row_max(float x) {
+  x = fmaxf(x, dpp_mov<kDppRowRor8>(x));
+  x = fmaxf(x, dpp_mov<kDppRowRor4>(x));
+  x = fmaxf(x, dpp_mov<kDppQuadXor2>(x));
+  x = fmaxf(x, dpp_mov<kDppQuadXor1>(x));
+  return x;
+}
+
 // 16 bytes from byte offset `off` of a buffer, read at device scope (coherent
 // across XCDs: the read does not hit a stale line of this XCD's L2); 0 when
 // `off` is past the buffer.
@@ -161,17 +172,34 @@ __device__ __forceinline__ void combine_group(const float* ws_m, const float* ws
     }
   }
   __syncthreads();
-  for (int r = threadIdx.x; r < nrows; r += NT) {
+  // Row weights: 16 lanes per row, lane j over partitions j, j + 16, ...; the
+  // row's maximum and sum are combined across its lanes with DPP moves, so no
+  // lane walks a row's partitions one after the other through LDS.
+  static_assert(NT % kRowLanes == 0, "whole rows of lanes");
+  constexpr int PPL = (kFusedMaxP + kRowLanes - 1) / kRowLanes;  // partitions per lane
+  const int j = (int)threadIdx.x % kRowLanes;
+  for (int r = (int)threadIdx.x / kRowLanes; r < nrows; r += NT / kRowLanes) {
+    float mloc[PPL];
     float M = kNegInf;
-    for (int p = 0; p < P; ++p) M = fmaxf(M, cw[r * P + p]);
+#pragma unroll
+    for (int k = 0; k < PPL; ++k) {
+      const int p = j + k * kRowLanes;
+      const float x = cw[r * P + min(p, P - 1)];  // clamped read; lanes past P count -inf
+      mloc[k] = p < P ? x : kNegInf;
+      M = fmaxf(M, mloc[k]);
+    }
+    M = row_max(M);
     const float ref = (M == kNegInf) ? 0.f : M;
     float L = 0.f;
-    for (int p = 0; p < P; ++p) {
-      const float w = exp2_fast((cw[r * P + p] - ref) * kLog2e);  // 0 for the identity
-      cw[r * P + p] = w;
-      L = fmaf(w, cl[r * P + p], L);
+#pragma unroll
+    for (int k = 0; k < PPL; ++k) {
+      const int p = j + k * kRowLanes;
+      const float w = exp2_fast((mloc[k] - ref) * kLog2e);  // 0 for the identity and past P
+      if (p < P) cw[r * P + p] = w;
+      L = fmaf(w, cl[r * P + min(p, P - 1)], L);
     }
-    cinv[r] = (M == kNegInf || L == 0.f) ? 0.f : 1.f / L;
+    L = group_sum<kRowLanes>(L);
+    if (j == 0) cinv[r] = (M == kNegInf || L == 0.f) ? 0.f : 1.f / L;
   }
   __syncthreads();
   for (int c0 = threadIdx.x; c0 < nslices; c0 += 2 * NT) {
